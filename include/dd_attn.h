@@ -1,0 +1,117 @@
+/*
+ * dd_attn.h -- C ABI of the dataset-decomposition attention hot path on
+ * MI355X (gfx950).
+ *
+ * The operation (Dataset Decomposition, arXiv 2405.13226):
+ *   A training step holds a fixed token budget.  Under dataset decomposition
+ *   it is B = budget / L sequences of length L = 2^i, each a piece of a single
+ *   document (Sec. 2.1 and 2.2).  Under the concat-and-chunk baseline it is
+ *   fixed-length chunks of concatenated documents, and document masking stops
+ *   a token from attending across a document boundary (Sec. 1; Sec. 3.6).  In
+ *   both cases the hot path is causal self-attention forward and backward,
+ *   where a token at context position j sees the j earlier tokens of its own
+ *   document and itself (Appendix F, eq. avg_context).
+ *
+ * Definition computed (softmax scale = 1/sqrt(D)), for row b, query i, key j:
+ *   allowed(i, j) = (!causal || j <= i) &&
+ *                   (cu_doclens == NULL || doc(b*L + i) == doc(b*L + j))
+ *   doc(t)        = the last k in [0, n_docs) with cu_doclens[k] <= t
+ *   O[b,i,h,:]    = sum_j softmax_j(scale * <Q[b,i,h,:], K[b,j,h,:]>) V[b,j,h,:]
+ *                   over allowed j
+ *   LSE[b,i,h]    = natural-log log-sum-exp of the allowed scaled scores
+ * The backward returns the gradients of sum(dO * O) with respect to Q, K, V.
+ * Attention never crosses a batch row; a document that spans a row edge is
+ * split there, as concat-and-chunk splits it.
+ *
+ * Layouts.  Q, K, V, O, dO, dQ, dK, dV: bf16, contiguous [B, L, H, D] with D
+ * innermost (token-major).  LSE: fp32, contiguous [B, L, H].  With this layout
+ * a document-masked [Bc, L] batch whose documents all have length l and the
+ * DD bucket batch [Bc*L/l, l] are the same bytes.
+ *
+ * Supported: D in {64, 128}; any L >= 1; B, H >= 1; B*L*H < 2^31.
+ * Arithmetic: bf16 inputs, fp32 accumulation (matrix cores), fp32 softmax
+ * statistics; probabilities and dS are rounded to bf16 before their products.
+ *
+ * Ownership.  Every tensor pointer is a DEVICE pointer owned by the caller,
+ * including the backward workspace.  The library allocates no device memory,
+ * keeps no pointer after a call returns and holds no state, so calls are
+ * thread-safe.  Work is enqueued asynchronously on `stream` (a hipStream_t;
+ * NULL = the default stream); outputs are valid once the caller synchronises.
+ *
+ * Errors.  Arguments are validated on the host before anything is enqueued;
+ * on error nothing is launched and outputs are untouched.  No exception
+ * crosses the ABI and nothing is printed.  The contents of cu_doclens live in
+ * device memory and are not read by the validator; callers check a host copy
+ * with dd_doclens_check().  Malformed contents cannot make a kernel access
+ * memory out of bounds, but results are then unspecified.
+ */
+#ifndef DD_ATTN_H
+#define DD_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DD_OK = 0,
+    DD_ERR_NULL = 1,      /* a required pointer is NULL                        */
+    DD_ERR_SHAPE = 2,     /* B, L or H < 1, or B*L*H >= 2^31                   */
+    DD_ERR_HEADDIM = 3,   /* D is not 64 or 128                                */
+    DD_ERR_DOCLENS = 4,   /* cu_doclens / n_docs inconsistent, or bad contents */
+    DD_ERR_WORKSPACE = 5, /* backward workspace missing or too small           */
+    DD_ERR_ALIGN = 6,     /* a tensor pointer is not 16-byte aligned (LSE: 4)  */
+    DD_ERR_ALIAS = 7,     /* an output overlaps an input or another output     */
+    DD_ERR_HIP = 8        /* the HIP runtime rejected a launch                 */
+} dd_status;
+
+/*
+ * Forward.  Q, K, V: inputs [B, L, H, D] bf16.  O: output [B, L, H, D] bf16.
+ * LSE: output [B, L, H] fp32, saved for the backward.
+ * causal: nonzero selects the causal mask (the method's setting); zero lets a
+ * query see its whole document (or row, without cu_doclens).
+ * cu_doclens: NULL with n_docs == 0 for no document mask; otherwise n_docs + 1
+ * int32 document start offsets over the flattened B*L token axis, with
+ * cu_doclens[0] == 0, strictly increasing, cu_doclens[n_docs] == B*L.
+ * stream: hipStream_t or NULL.  Returns a dd_status.
+ */
+int dd_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                int B, int L, int H, int D, int causal,
+                const int32_t *cu_doclens, int n_docs, void *stream);
+
+/*
+ * Backward of sum(dO * O) for the forward above (same Q, K, V, mask), given
+ * its outputs O and LSE and the upstream gradient dO, all as laid out above.
+ * dQ, dK, dV: outputs [B, L, H, D] bf16; every element is written.
+ * workspace: device scratch of at least dd_attn_bwd_workspace_bytes(B, L, H, D)
+ * bytes, 16-byte aligned, owned by the caller; its contents on entry are
+ * ignored and on return are unspecified.  It must not overlap any tensor.
+ * Returns a dd_status.
+ */
+int dd_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
+                const void *dO, const float *LSE, void *dQ, void *dK, void *dV,
+                int B, int L, int H, int D, int causal,
+                const int32_t *cu_doclens, int n_docs,
+                void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes dd_attn_bwd needs for this shape (0 for an invalid shape). */
+size_t dd_attn_bwd_workspace_bytes(int B, int L, int H, int D);
+
+/*
+ * Checks a HOST copy of cu_doclens: n_docs >= 1, cu[0] == 0, strictly
+ * increasing, cu[n_docs] == total_tokens.  Returns DD_OK or DD_ERR_DOCLENS
+ * (DD_ERR_NULL for a NULL pointer).
+ */
+int dd_doclens_check(const int32_t *host_cu_doclens, int n_docs,
+                     long long total_tokens);
+
+/* Static English text of a status code ("unknown status" otherwise). */
+const char *dd_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DD_ATTN_H */

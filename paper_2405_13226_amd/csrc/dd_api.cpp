@@ -1,0 +1,175 @@
+// dd_api.cpp -- the C ABI entry points declared in include/dd_attn.h.
+//
+// Host-only C++: argument validation, workspace sizing and status strings.
+// Nothing here touches the GPU; the launches live in dd_fwd.hip and
+// dd_bwd.hip behind the internal interface of dd_internal.h.  Every check
+// runs before any launch, so an invalid call leaves all outputs untouched.
+#include "dd_attn.h"
+#include "dd_internal.h"
+
+#include <cstdint>
+#include <initializer_list>
+
+namespace {
+
+struct Range {
+    uintptr_t lo, hi;  // [lo, hi)
+};
+
+Range range_of(const void *p, size_t bytes)
+{
+    uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    return Range{a, a + bytes};
+}
+
+bool overlaps(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+bool aligned(const void *p, uintptr_t n)
+{
+    return (reinterpret_cast<uintptr_t>(p) & (n - 1)) == 0;
+}
+
+int check_shape(int B, int L, int H, int D)
+{
+    if (B < 1 || L < 1 || H < 1)
+        return DD_ERR_SHAPE;
+    long long rows = static_cast<long long>(B) * L * H;
+    if (rows >= (1LL << 31))
+        return DD_ERR_SHAPE;
+    if (D != 64 && D != 128)
+        return DD_ERR_HEADDIM;
+    return DD_OK;
+}
+
+int check_doc_args(const int32_t *cu, int n_docs, int B, int L)
+{
+    if ((cu == nullptr) != (n_docs == 0))
+        return DD_ERR_DOCLENS;
+    if (cu != nullptr) {
+        if (n_docs < 1 || static_cast<long long>(n_docs) > static_cast<long long>(B) * L)
+            return DD_ERR_DOCLENS;
+        if (!aligned(cu, 4))
+            return DD_ERR_ALIGN;
+    }
+    return DD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t dd_attn_bwd_workspace_bytes(int B, int L, int H, int D)
+{
+    if (check_shape(B, L, H, D) != DD_OK)
+        return 0;
+    return dd::bwd_workspace_bytes(B, L, H);
+}
+
+int dd_doclens_check(const int32_t *cu, int n_docs, long long total_tokens)
+{
+    if (cu == nullptr)
+        return DD_ERR_NULL;
+    if (n_docs < 1 || total_tokens < 1 || cu[0] != 0)
+        return DD_ERR_DOCLENS;
+    for (int k = 0; k < n_docs; ++k)
+        if (cu[k + 1] <= cu[k])
+            return DD_ERR_DOCLENS;
+    if (static_cast<long long>(cu[n_docs]) != total_tokens)
+        return DD_ERR_DOCLENS;
+    return DD_OK;
+}
+
+const char *dd_status_str(int status)
+{
+    switch (status) {
+    case DD_OK: return "ok";
+    case DD_ERR_NULL: return "a required pointer is NULL";
+    case DD_ERR_SHAPE: return "invalid shape: need B, L, H >= 1 and B*L*H < 2^31";
+    case DD_ERR_HEADDIM: return "unsupported head dimension: D must be 64 or 128";
+    case DD_ERR_DOCLENS: return "invalid cu_doclens / n_docs";
+    case DD_ERR_WORKSPACE: return "backward workspace missing or too small";
+    case DD_ERR_ALIGN: return "misaligned pointer: tensors need 16-byte alignment";
+    case DD_ERR_ALIAS: return "an output buffer overlaps another buffer";
+    case DD_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+    }
+}
+
+int dd_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                int B, int L, int H, int D, int causal,
+                const int32_t *cu_doclens, int n_docs, void *stream)
+{
+    if (!Q || !K || !V || !O || !LSE)
+        return DD_ERR_NULL;
+    int st = check_shape(B, L, H, D);
+    if (st != DD_OK)
+        return st;
+    st = check_doc_args(cu_doclens, n_docs, B, L);
+    if (st != DD_OK)
+        return st;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
+        !aligned(LSE, 4))
+        return DD_ERR_ALIGN;
+    const size_t tb = static_cast<size_t>(B) * L * H * D * 2;
+    const size_t lb = static_cast<size_t>(B) * L * H * 4;
+    Range rq = range_of(Q, tb), rk = range_of(K, tb), rv = range_of(V, tb);
+    Range ro = range_of(O, tb), rl = range_of(LSE, lb);
+    for (Range in : {rq, rk, rv})
+        if (overlaps(ro, in) || overlaps(rl, in))
+            return DD_ERR_ALIAS;
+    if (overlaps(ro, rl))
+        return DD_ERR_ALIAS;
+    if (cu_doclens) {
+        Range rc = range_of(cu_doclens, static_cast<size_t>(n_docs + 1) * 4);
+        if (overlaps(rc, ro) || overlaps(rc, rl))
+            return DD_ERR_ALIAS;
+    }
+    dd::FwdArgs a{Q, K, V, O, LSE, B, L, H, D, causal != 0, cu_doclens, n_docs, stream};
+    return dd::launch_fwd(a);
+}
+
+int dd_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
+                const void *dO, const float *LSE, void *dQ, void *dK, void *dV,
+                int B, int L, int H, int D, int causal,
+                const int32_t *cu_doclens, int n_docs,
+                void *workspace, size_t workspace_bytes, void *stream)
+{
+    if (!Q || !K || !V || !O || !dO || !LSE || !dQ || !dK || !dV)
+        return DD_ERR_NULL;
+    int st = check_shape(B, L, H, D);
+    if (st != DD_OK)
+        return st;
+    st = check_doc_args(cu_doclens, n_docs, B, L);
+    if (st != DD_OK)
+        return st;
+    const size_t need = dd::bwd_workspace_bytes(B, L, H);
+    if (!workspace || workspace_bytes < need)
+        return DD_ERR_WORKSPACE;
+    for (const void *p : {Q, K, V, O, dO, static_cast<const void *>(dQ),
+                          static_cast<const void *>(dK), static_cast<const void *>(dV),
+                          static_cast<const void *>(workspace)})
+        if (!aligned(p, 16))
+            return DD_ERR_ALIGN;
+    if (!aligned(LSE, 4))
+        return DD_ERR_ALIGN;
+    const size_t tb = static_cast<size_t>(B) * L * H * D * 2;
+    const size_t lb = static_cast<size_t>(B) * L * H * 4;
+    Range ins[] = {range_of(Q, tb), range_of(K, tb), range_of(V, tb), range_of(O, tb),
+                   range_of(dO, tb), range_of(LSE, lb),
+                   range_of(cu_doclens, cu_doclens ? static_cast<size_t>(n_docs + 1) * 4 : 0)};
+    Range outs[] = {range_of(dQ, tb), range_of(dK, tb), range_of(dV, tb),
+                    range_of(workspace, need)};
+    for (int i = 0; i < 4; ++i) {
+        for (Range in : ins)
+            if (overlaps(outs[i], in))
+                return DD_ERR_ALIAS;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlaps(outs[i], outs[j]))
+                return DD_ERR_ALIAS;
+    }
+    dd::BwdArgs a{Q, K, V, O, dO, LSE, dQ, dK, dV, B, L, H, D, causal != 0,
+                  cu_doclens, n_docs, workspace, stream};
+    return dd::launch_bwd(a);
+}
+
+}  // extern "C"

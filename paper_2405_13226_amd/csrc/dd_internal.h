@@ -1,0 +1,46 @@
+// dd_internal.h -- interface between the validated C ABI (dd_api.cpp) and the
+// HIP launchers (dd_fwd.hip, dd_bwd.hip).  Host-only declarations: no HIP
+// types, so the validation unit stays plain C++.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+namespace dd {
+
+struct FwdArgs {
+    const void *Q, *K, *V;
+    void *O;
+    float *LSE;
+    int B, L, H, D;
+    bool causal;
+    const int32_t *cu;
+    int n_docs;
+    void *stream;
+};
+
+struct BwdArgs {
+    const void *Q, *K, *V, *O, *dO;
+    const float *LSE;
+    void *dQ, *dK, *dV;
+    int B, L, H, D;
+    bool causal;
+    const int32_t *cu;
+    int n_docs;
+    void *workspace;
+    void *stream;
+};
+
+// Backward scratch: per (b, h) row, LSE in log2 units and delta = rowsum(dO*O),
+// both fp32 [B*H][L], each region 256-byte aligned.
+inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+inline size_t bwd_workspace_bytes(int B, int L, int H)
+{
+    return 2 * align256(static_cast<size_t>(B) * H * L * sizeof(float));
+}
+
+// Both return a dd_status value (DD_OK or DD_ERR_HIP).
+int launch_fwd(const FwdArgs &a);
+int launch_bwd(const BwdArgs &a);
+
+}  // namespace dd

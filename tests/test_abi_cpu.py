@@ -1,0 +1,149 @@
+"""The C ABI without a GPU: the library loads, exports every function the
+header declares, and rejects every invalid call before launching anything
+(validation runs on the host, so these calls never reach the device)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2405_13226_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dd_attn.h")
+
+OK, NULL, SHAPE, HEADDIM, DOCLENS, WORKSPACE, ALIGN, ALIAS = range(8)
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dd_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.fail("libdd_attn.so is not built (python -m paper_2405_13226_amd.build)")
+    return _lib.lib()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = header_functions()
+    assert set(names) == set(_lib.SIGNATURES), names
+    raw = ctypes.CDLL(_lib.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+def test_status_strings(lib):
+    for code in range(9):
+        s = lib.dd_status_str(code)
+        assert s and s != b"unknown status"
+    assert lib.dd_status_str(99) == b"unknown status"
+    assert lib.dd_status_str(OK) == b"ok"
+
+
+def test_workspace_bytes(lib):
+    n = lib.dd_attn_bwd_workspace_bytes(8, 8192, 16, 128)
+    rows = 8 * 8192 * 16 * 4
+    assert n >= 2 * rows and n % 256 == 0
+    assert lib.dd_attn_bwd_workspace_bytes(1, 1, 1, 64) == 512
+    assert lib.dd_attn_bwd_workspace_bytes(1, 1, 1, 80) == 0
+    assert lib.dd_attn_bwd_workspace_bytes(0, 1, 1, 64) == 0
+
+
+def doc_check(lib, cu, total):
+    a = np.ascontiguousarray(np.asarray(cu, dtype=np.int32))
+    return lib.dd_doclens_check(a.ctypes.data_as(ctypes.c_void_p), a.size - 1, total)
+
+
+def test_doclens_check(lib):
+    assert doc_check(lib, [0, 5, 9, 16], 16) == OK
+    assert doc_check(lib, [0, 16], 16) == OK
+    assert doc_check(lib, [1, 5, 16], 16) == DOCLENS
+    assert doc_check(lib, [0, 5, 5, 16], 16) == DOCLENS
+    assert doc_check(lib, [0, 7, 3, 16], 16) == DOCLENS
+    assert doc_check(lib, [0, 5, 15], 16) == DOCLENS
+    assert doc_check(lib, [0], 16) == DOCLENS
+    assert lib.dd_doclens_check(None, 3, 16) == NULL
+
+
+# Fake, 16-byte aligned, non-overlapping device addresses: validation fails
+# before any of them could be dereferenced or a kernel launched.
+BASE = 1 << 40
+GAP = 1 << 34
+
+
+def fake(i, off=0):
+    return ctypes.c_void_p(BASE + i * GAP + off)
+
+
+def fwd(lib, q=None, k=None, v=None, o=None, lse=None, B=2, L=64, H=2, D=64, causal=1,
+        cu=None, n_docs=0):
+    args = [q or fake(0), k or fake(1), v or fake(2), o or fake(3), lse or fake(4)]
+    return lib.dd_attn_fwd(*args, B, L, H, D, causal, cu, n_docs, None)
+
+
+def test_fwd_validation(lib):
+    assert lib.dd_attn_fwd(None, fake(1), fake(2), fake(3), fake(4), 2, 64, 2, 64, 1,
+                           None, 0, None) == NULL
+    assert lib.dd_attn_fwd(fake(0), fake(1), fake(2), fake(3), None, 2, 64, 2, 64, 1,
+                           None, 0, None) == NULL
+    assert fwd(lib, B=0) == SHAPE
+    assert fwd(lib, L=0) == SHAPE
+    assert fwd(lib, H=-1) == SHAPE
+    assert fwd(lib, B=1 << 16, L=1 << 15, H=1) == SHAPE
+    assert fwd(lib, D=80) == HEADDIM
+    assert fwd(lib, D=32) == HEADDIM
+    assert fwd(lib, cu=fake(5), n_docs=0) == DOCLENS
+    assert fwd(lib, cu=None, n_docs=3) == DOCLENS
+    assert fwd(lib, cu=fake(5), n_docs=129) == DOCLENS
+    assert fwd(lib, cu=fake(5, 2), n_docs=3) == ALIGN
+    assert fwd(lib, q=fake(0, 8)) == ALIGN
+    assert fwd(lib, o=fake(3, 4)) == ALIGN
+    assert fwd(lib, lse=fake(4, 2)) == ALIGN
+    assert fwd(lib, o=fake(0, 64)) == ALIAS          # O overlaps Q
+    assert fwd(lib, lse=fake(3, 1024)) == ALIAS      # LSE inside O
+    assert fwd(lib, o=fake(5), lse=fake(5, 16)) == ALIAS
+    assert fwd(lib, cu=fake(3, 32), n_docs=2) == ALIAS
+
+
+def bwd(lib, ptrs=None, B=2, L=64, H=2, D=64, cu=None, n_docs=0, ws=None, ws_bytes=None):
+    p = [fake(i) for i in range(9)]
+    if ptrs:
+        for i, v in ptrs.items():
+            p[i] = v
+    need = lib.dd_attn_bwd_workspace_bytes(B, L, H, D)
+    ws = ws if ws is not None else fake(9)
+    return lib.dd_attn_bwd(*p, B, L, H, D, 1, cu, n_docs, ws,
+                           need if ws_bytes is None else ws_bytes, None)
+
+
+def test_bwd_validation(lib):
+    for i in range(9):
+        assert bwd(lib, {i: None}) == NULL, i
+    assert bwd(lib, B=0) == SHAPE
+    assert bwd(lib, D=96) == HEADDIM
+    assert bwd(lib, cu=fake(10), n_docs=0) == DOCLENS
+    assert bwd(lib, ws=ctypes.c_void_p(0)) == WORKSPACE
+    assert bwd(lib, ws_bytes=100) == WORKSPACE
+    assert bwd(lib, {0: fake(0, 8)}) == ALIGN
+    assert bwd(lib, {5: fake(5, 2)}) == ALIGN
+    assert bwd(lib, ws=fake(9, 8)) == ALIGN
+    assert bwd(lib, {7: fake(6)}) == ALIAS            # dK == dQ
+    assert bwd(lib, {6: fake(4, 16)}) == ALIAS        # dQ overlaps dO
+    assert bwd(lib, ws=fake(8, 1024)) == ALIAS        # workspace inside dV
+    assert bwd(lib, {8: fake(5)}) == ALIAS            # dV over LSE
+    assert bwd(lib, cu=fake(7, 64), n_docs=2) == ALIAS
+
+
+def test_python_wrapper_checks_metadata_on_cpu():
+    torch = pytest.importorskip("torch")
+    import paper_2405_13226_amd as dd
+    q = torch.zeros(1, 4, 1, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        dd.forward(q, q, q)  # CPU tensors are rejected before any call
+    with pytest.raises(_lib.DDError):
+        dd.DocLens([0, 3, 2, 4], 4, torch.device("cpu"))

@@ -1,0 +1,159 @@
+"""GPU checks of properties the method fixes, independent of the oracle.
+
+* a length-1 sequence returns V bit for bit (and dV = dO bit for bit);
+* causality: perturbing the future leaves earlier outputs bit for bit equal
+  (masked probabilities are exact zeros);
+* constant V returns that constant;
+* DD buckets and document-masked chunks of equal-length documents are the
+  same bytes, so both calls give the same outputs (Sec. 2.1 / Sec. 3.6);
+* a masked chunk equals separate calls per document;
+* gradients of the keys sum to zero per document;
+* repeated calls are bitwise deterministic (no atomics anywhere);
+* the autograd wrapper matches the explicit backward.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+import paper_2405_13226_amd as dd
+
+from parity import log, rel_l2, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def inputs(B, L, H, D, seed, dev):
+    x = synth.attention_inputs(B, L, H, D, seed=seed)
+    return {n: to_dev(a, dev) for n, a in x.items()}
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_length_one_returns_v_bitwise(cuda, D):
+    x = inputs(37, 1, 5, D, 1, cuda)
+    o, lse = dd.forward(x["q"], x["k"], x["v"])
+    assert torch.equal(o.view(torch.int16), x["v"].view(torch.int16))
+    scale = 1.0 / np.sqrt(D)
+    ref = (x["q"].float() * x["k"].float()).sum(-1) * scale
+    assert torch.allclose(lse, ref, atol=1e-4)
+    dq, dk, dv = dd.backward(x["q"], x["k"], x["v"], o, lse, x["do"])
+    assert torch.equal(dv.view(torch.int16), x["do"].view(torch.int16))
+    # dS = P (dP - delta) is zero in exact arithmetic; in fp32, delta and dP
+    # are summed in different orders, leaving rounding-level residue.
+    assert dq.float().abs().max().item() <= 1e-5
+    assert dk.float().abs().max().item() <= 1e-5
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_future_perturbation_bitwise(cuda, D):
+    B, L, H = 2, 777, 2
+    x = inputs(B, L, H, D, 2, cuda)
+    o1, l1 = dd.forward(x["q"], x["k"], x["v"])
+    cut = 400
+    k2, v2, q2 = x["k"].clone(), x["v"].clone(), x["q"].clone()
+    k2[:, cut:] = -k2[:, cut:]
+    v2[:, cut:] = v2[:, cut:] * 2
+    q2[:, cut:] = 0
+    o2, l2 = dd.forward(q2, k2, v2)
+    assert torch.equal(o1[:, :cut].view(torch.int16), o2[:, :cut].view(torch.int16))
+    assert torch.equal(l1[:, :cut], l2[:, :cut])
+    assert not torch.equal(o1[:, cut:], o2[:, cut:])
+
+
+def test_constant_v(cuda):
+    B, L, H, D = 2, 1000, 2, 128
+    x = inputs(B, L, H, D, 3, cuda)
+    v = torch.ones_like(x["v"])
+    o, _ = dd.forward(x["q"], x["k"], v, cu_doclens=[0, 10, 700, 2000])
+    assert (o.float() - 1).abs().max().item() <= 1e-2
+
+
+@pytest.mark.parametrize("ell", [64, 256, 1024])
+def test_dd_buckets_equal_masked_chunks(cuda, ell):
+    Bc, L, H, D = 2, 2048, 4, 64
+    x = inputs(Bc, L, H, D, 4, cuda)
+    cu = np.arange(0, Bc * L + 1, ell)
+    o1, l1 = dd.forward(x["q"], x["k"], x["v"], cu_doclens=cu)
+    g1 = dd.backward(x["q"], x["k"], x["v"], o1, l1, x["do"], cu_doclens=cu)
+    r = {n: t.view(Bc * L // ell, ell, H, D) for n, t in x.items()}
+    o2, l2 = dd.forward(r["q"], r["k"], r["v"])
+    g2 = dd.backward(r["q"], r["k"], r["v"], o2, l2, r["do"])
+    same = torch.equal(o1.view(-1), o2.view(-1))
+    log(f"  ell={ell}: forward bitwise equal = {same}")
+    assert (o1.view(-1).float() - o2.view(-1).float()).abs().max().item() <= 1e-2
+    assert (l1.view(-1) - l2.view(-1)).abs().max().item() <= 1e-4
+    for a, b in zip(g1, g2):
+        assert rel_l2(a.float().cpu().numpy().ravel(), b.float().cpu().numpy().ravel()) <= 1e-2
+
+
+def test_masked_chunk_equals_separate_documents(cuda):
+    B, L, H, D = 2, 1024, 2, 128
+    lens = synth.lognormal_doc_lengths(8, total_tokens=B * L, median=200)
+    cu = dd.dd.chunk_doclens(lens, B * L)
+    x = inputs(B, L, H, D, 5, cuda)
+    o, lse = dd.forward(x["q"], x["k"], x["v"], cu_doclens=cu)
+    flat = {n: t.view(B * L, H, D) for n, t in x.items()}
+    of, lf = o.view(B * L, H, D), lse.view(B * L, H)
+    edges = sorted(set(cu.tolist()) | set(range(0, B * L + 1, L)))
+    worst = 0.0
+    for a, z in zip(edges[:-1], edges[1:]):
+        seg = {n: t[a:z].unsqueeze(0).contiguous() for n, t in flat.items()}
+        od, ld = dd.forward(seg["q"], seg["k"], seg["v"])
+        worst = max(worst, (od[0].float() - of[a:z].float()).abs().max().item())
+        assert (ld[0] - lf[a:z]).abs().max().item() <= 1e-4
+    assert worst <= 1e-2
+
+
+def test_key_gradients_sum_to_zero_per_document(cuda):
+    B, L, H, D = 2, 1536, 2, 64
+    lens = synth.lognormal_doc_lengths(9, total_tokens=B * L, median=300)
+    cu = dd.dd.chunk_doclens(lens, B * L)
+    x = inputs(B, L, H, D, 6, cuda)
+    o, lse = dd.forward(x["q"], x["k"], x["v"], cu_doclens=cu)
+    _, dk, _ = dd.backward(x["q"], x["k"], x["v"], o, lse, x["do"], cu_doclens=cu)
+    dkf = dk.float().view(B * L, H, D)
+    edges = sorted(set(cu.tolist()) | set(range(0, B * L + 1, L)))
+    for a, z in zip(edges[:-1], edges[1:]):
+        s = dkf[a:z].sum(0).abs().max().item()
+        scale = dkf[a:z].abs().sum(0).max().item() + 1e-6
+        assert s <= 2e-2 * scale + 1e-3, (a, z, s, scale)
+
+
+def test_repeat_calls_are_bitwise_deterministic(cuda):
+    B, L, H, D = 4, 1024, 4, 128
+    x = inputs(B, L, H, D, 7, cuda)
+    outs = []
+    for _ in range(2):
+        o, lse = dd.forward(x["q"], x["k"], x["v"])
+        g = dd.backward(x["q"], x["k"], x["v"], o, lse, x["do"])
+        outs.append([o, lse, *g])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+def test_autograd_wrapper(cuda):
+    B, L, H, D = 2, 300, 2, 64
+    x = inputs(B, L, H, D, 8, cuda)
+    q, k, v = (x[n].clone().requires_grad_(True) for n in ("q", "k", "v"))
+    o = dd.attention(q, k, v, True, [0, 100, 350, 600])
+    o.backward(x["do"])
+    o2, lse = dd.forward(x["q"], x["k"], x["v"], cu_doclens=[0, 100, 350, 600])
+    g = dd.backward(x["q"], x["k"], x["v"], o2, lse, x["do"], cu_doclens=[0, 100, 350, 600])
+    assert torch.equal(o, o2)
+    for a, b in zip((q.grad, k.grad, v.grad), g):
+        assert torch.equal(a, b)
+
+
+def test_errors_with_live_device(cuda):
+    x = inputs(1, 64, 1, 64, 9, cuda)
+    bad = torch.zeros(1, 64, 1, 80, dtype=torch.bfloat16, device=cuda)
+    with pytest.raises(dd.DDError):
+        dd.forward(bad, bad, bad)
+    with pytest.raises(dd.DDError):
+        dd.forward(x["q"], x["k"], x["v"], cu_doclens=[0, 10, 5, 64])
+    o = torch.empty_like(x["q"])
+    lse = torch.empty(1, 64, 1, device=cuda)
+    st = dd.lib().dd_attn_fwd(x["q"].data_ptr(), x["k"].data_ptr(), x["v"].data_ptr(),
+                              x["q"].data_ptr(), lse.data_ptr(), 1, 64, 1, 64, 1, None, 0, None)
+    assert st == 7  # O aliases Q
+    del o

@@ -1,0 +1,69 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Small cases compare every element; the full 65,536-token buckets compare all
+rows of sampled (b, h) pairs, which is exact parity for those pairs because
+pairs are independent.  Tolerances are in tests/parity.py.
+"""
+import numpy as np
+import pytest
+
+import synth
+from paper_2405_13226_amd import dd
+
+from parity import check_case, log
+
+pytestmark = pytest.mark.gpu
+
+
+def test_tiny_config_full_parity(cuda):
+    # B=4 sequences x L=256, H=4, D=64, causal: every output element.
+    _, _, res = check_case(4, 256, 4, 64, causal=True, seed=0, tag="tiny")
+    assert res["o_maxabs"] <= 1e-2
+
+
+@pytest.mark.parametrize("B,L,H,D,causal", [
+    (1, 1, 1, 64, True), (3, 1, 2, 128, True), (2, 7, 3, 64, True), (1, 100, 2, 128, True),
+    (2, 129, 1, 64, True), (1, 300, 2, 128, True), (2, 64, 2, 64, False),
+    (1, 200, 1, 128, False), (1, 513, 1, 64, True), (2, 384, 2, 128, True)])
+def test_ragged_shapes(cuda, B, L, H, D, causal):
+    check_case(B, L, H, D, causal=causal, seed=B * 1000 + L)
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("causal", [True, False])
+def test_document_masked_chunks(cuda, D, causal):
+    # Concat-and-chunk rows of 512 with short and row-crossing documents.
+    B, L, H = 3, 512, 2
+    lens = synth.lognormal_doc_lengths(5, total_tokens=B * L, median=150, sigma=1.0)
+    cu = dd.chunk_doclens(lens, B * L)
+    check_case(B, L, H, D, causal=causal, cu=cu, seed=D + causal)
+
+
+def test_single_token_documents(cuda):
+    B, L, H, D = 1, 130, 1, 64
+    cu = np.arange(0, B * L + 1)
+    check_case(B, L, H, D, cu=cu, seed=3)
+
+
+@pytest.mark.parametrize("L,D", [(256, 64), (1024, 64), (8192, 64), (256, 128), (2048, 128),
+                                 (8192, 128)])
+def test_full_step_buckets_sampled(cuda, L, D):
+    # A 65,536-token step: B = 65536 / L sequences, H = 16.
+    B, H = 65536 // L, 16
+    bh = [(0, 0), (B - 1, H - 1), (B // 2, 7)]
+    check_case(B, L, H, D, causal=True, seed=0, bh=bh, tag=f"bucket L={L} D={D}")
+
+
+def test_concat_chunk_step_sampled(cuda):
+    # 8 chunks x 8192 tokens of log-normal documents, document-masked.
+    B, L, H, D = 8, 8192, 16, 64
+    lens = synth.lognormal_doc_lengths(0)
+    cu = dd.chunk_doclens(lens, B * L)
+    check_case(B, L, H, D, causal=True, cu=cu, seed=0, bh=[(0, 0), (5, 9), (7, 15)],
+               tag="chunk 8x8192 masked")
+
+
+def test_longest_bucket_sampled(cuda):
+    B, L, H, D = 4, 16384, 16, 128
+    check_case(B, L, H, D, causal=True, seed=0, bh=[(3, 15)], tag="bucket L=16384 D=128")
+    log("done")
