@@ -1,0 +1,323 @@
+#!/usr/bin/env python3
+"""Benchmark of the dataset-decomposition attention hot path on one MI355X.
+
+A bench step runs causal attention forward + backward (through the C ABI)
+over every launch group of the chosen workload; each group is one
+65,536-token training step, so per group B * L = 65536.
+
+Workloads (``--workload``):
+  dd_sweep_d64   (default) buckets L = 256 .. 8192, B = 65536 / L, H = 16, D = 64
+  dd_sweep_d128  the same with D = 128
+  chunk_vs_dd    8 x 8192 chunks of log-normal documents: dense causal,
+                 document-masked, and the DD buckets of the same documents
+  stream         64 steps with L drawn from 256 .. 16384, weights 1/L, D = 128
+  tiny           B = 4, L = 256, H = 4, D = 64
+
+Prints ONE JSON line on stdout: the metric is useful attention TFLOP/s
+(forward 4*D and backward 10*D FLOPs per allowed (query, key) pair and head)
+over the whole bench step, with per-group times, tokens/s, the roofline of
+the dominant kernel (timed with HIP events on its own stream) and the fp64
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+TOKENS = 65536
+BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+METRIC = "attention fwd+bwd TFLOP/s and tokens/s per bucket at 65,536 tokens/step"
+BUCKETS = [256, 512, 1024, 2048, 4096, 8192]
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="dd_sweep_d64",
+                    choices=["dd_sweep_d64", "dd_sweep_d128", "chunk_vs_dd", "stream", "tiny"])
+    ap.add_argument("--buckets", default=None,
+                    help="comma-separated subset of bucket lengths (sweeps only)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle sample")
+    ap.add_argument("--events", default="inline", choices=["inline", "separate"],
+                    help="time groups/kernels with events inside the timed region, or in "
+                         "a second pass after a clean one")
+    ap.add_argument("--traffic", default=None,
+                    help="JSON file of measured HBM bytes per launch for the dominant kernel")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+# workloads: a list of launch groups {name, B, L, cu (host int32 or None)}
+# ---------------------------------------------------------------------------
+def workload(name, seed, buckets=None):
+    import numpy as np
+    import synth
+    from paper_2405_13226_amd import dd
+
+    if name in ("dd_sweep_d64", "dd_sweep_d128"):
+        H, D = 16, 64 if name.endswith("64") else 128
+        lens = buckets or BUCKETS
+        groups = [dict(name=f"L={L}", B=TOKENS // L, L=L, cu=None) for L in lens]
+        desc = dict(workload=name, tokens_per_group=TOKENS, buckets=lens, H=H, D=D,
+                    causal=True)
+    elif name == "tiny":
+        H, D = 4, 64
+        groups = [dict(name="L=256", B=4, L=256, cu=None)]
+        desc = dict(workload=name, tokens_per_group=1024, buckets=[256], H=H, D=D, causal=True)
+    elif name == "chunk_vs_dd":
+        H, D = 16, 64
+        docs = synth.lognormal_doc_lengths(seed, TOKENS)
+        cu = dd.chunk_doclens(docs, TOKENS)
+        groups = [dict(name="dense 8x8192", B=8, L=8192, cu=None, variant="dense"),
+                  dict(name="masked 8x8192", B=8, L=8192, cu=cu, variant="masked")]
+        for n, b in dd.decompose(docs, min_len=256, max_len=8192).items():
+            groups.append(dict(name=f"DD L={n}", B=b.count, L=n, cu=None, variant="dd"))
+        desc = dict(workload=name, tokens_per_group=TOKENS, H=H, D=D, causal=True,
+                    documents=int(len(docs)), doc_seed=seed,
+                    dd_tokens_kept=int(sum(g["B"] * g["L"] for g in groups
+                                           if g.get("variant") == "dd")))
+    else:  # stream
+        H, D = 16, 128
+        lens = synth.length_stream(seed, steps=64)
+        groups = [dict(name=f"step{i} L={int(L)}", B=TOKENS // int(L), L=int(L), cu=None)
+                  for i, L in enumerate(lens)]
+        desc = dict(workload=name, tokens_per_group=TOKENS, steps_per_stream=64, H=H, D=D,
+                    causal=True, lengths={int(k): int(v) for k, v in
+                                          zip(*np.unique(lens, return_counts=True))})
+    for g in groups:
+        g["H"], g["D"] = H, D
+        f, b = dd.attention_flops(g["B"], g["L"], H, D, True, g["cu"])
+        g["flops_fwd"], g["flops_bwd"] = f, b
+        g["pairs"] = dd.useful_pairs(g["B"], g["L"], True, g["cu"]) * H
+        g["tokens"] = g["B"] * g["L"]
+    return groups, desc
+
+
+# ---------------------------------------------------------------------------
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the attention "
+              "path has no cross-GPU exchange and this build measures a single MI355X.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2405_13226_amd as ddlib
+    from paper_2405_13226_amd import _lib
+
+    lib = ddlib.lib()  # raises if the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    buckets = [int(x) for x in args.buckets.split(",")] if args.buckets else None
+    groups, desc = workload(args.workload, args.seed, buckets)
+    H, D = desc["H"], desc["D"]
+    ntok = max(g["tokens"] for g in groups)
+
+    # Resident inputs (seeded N(0,1) bf16) and outputs, sized for the largest group.
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    shape = (ntok, H, D)
+    q, k, v, do = (torch.randn(shape, generator=gen, device=dev, dtype=torch.float32)
+                   .to(torch.bfloat16) for _ in range(4))
+    o = torch.empty_like(q)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    lse = torch.empty((ntok, H), dtype=torch.float32, device=dev)
+    ws_bytes = max(ddlib.workspace_bytes(g["B"], g["L"], H, D) for g in groups)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    for g in groups:
+        g["docs"] = ddlib.DocLens(g["cu"], g["tokens"], dev) if g["cu"] is not None else None
+    P = ctypes.c_void_p
+    ptr = {n: P(t.data_ptr()) for n, t in dict(q=q, k=k, v=v, do=do, o=o, dq=dq, dk=dk, dv=dv,
+                                                lse=lse, ws=ws).items()}
+    stream = torch.cuda.current_stream(dev)
+    sptr = P(stream.cuda_stream)
+
+    def run_group(g, mark=False):
+        B, L = g["B"], g["L"]
+        cu = P(g["docs"].dev.data_ptr()) if g["docs"] else None
+        nd = g["docs"].n_docs if g["docs"] else 0
+        st = lib.dd_attn_fwd(ptr["q"], ptr["k"], ptr["v"], ptr["o"], ptr["lse"], B, L, H, D, 1,
+                             cu, nd, sptr)
+        _lib.check(st, "dd_attn_fwd")
+        if mark:
+            g["ev"][1].record(stream)
+        st = lib.dd_attn_bwd(ptr["q"], ptr["k"], ptr["v"], ptr["o"], ptr["do"], ptr["lse"],
+                             ptr["dq"], ptr["dk"], ptr["dv"], B, L, H, D, 1, cu, nd,
+                             ptr["ws"], ws_bytes, sptr)
+        _lib.check(st, "dd_attn_bwd")
+
+    def new_events():
+        return [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+
+    log(f"workload {desc['workload']}: {len(groups)} groups, H={H} D={D}")
+    for g in groups:
+        g["ev"] = new_events()
+    for _ in range(args.warmup):
+        for g in groups:
+            run_group(g)
+    torch.cuda.synchronize(dev)
+
+    def timed(with_events):
+        """K bench steps; returns wall seconds.  With events, every group is
+        bracketed by torch events and every library kernel by the library's
+        own HIP event pair on the same stream."""
+        if with_events:
+            for g in groups:
+                g["evs"] = [new_events() for _ in range(args.steps)]
+            _lib.prof_enable(True)
+        torch.cuda.synchronize(dev)
+        t0 = time.perf_counter()
+        for s in range(args.steps):
+            for g in groups:
+                if with_events:
+                    g["ev"] = g["evs"][s]
+                    g["ev"][0].record(stream)
+                run_group(g, with_events)
+                if with_events:
+                    g["ev"][2].record(stream)
+        torch.cuda.synchronize(dev)
+        wall = time.perf_counter() - t0
+        if with_events:
+            _lib.prof_enable(False)
+        return wall
+
+    wall = timed(args.events == "inline")
+    if args.events == "separate":
+        wall_ev = timed(True)
+        log(f"wall per step: {wall * 1e3 / args.steps:.3f} ms clean, "
+            f"{wall_ev * 1e3 / args.steps:.3f} ms with events")
+
+    ms_per_step = wall * 1e3 / args.steps
+    flops_step = sum(g["flops_fwd"] + g["flops_bwd"] for g in groups)
+    tokens_step = sum(g["tokens"] for g in groups)
+    value = flops_step / (ms_per_step * 1e-3) / 1e12
+
+    per_group = []
+    for g in groups:
+        f = [e[0].elapsed_time(e[1]) for e in g["evs"]]
+        b = [e[1].elapsed_time(e[2]) for e in g["evs"]]
+        fm, bm = float(np.mean(f)), float(np.mean(b))
+        tot = fm + bm
+        fb, bb = ddlib.dd.attention_bytes(g["B"], g["L"], H, D)
+        rec = dict(name=g["name"], B=g["B"], L=g["L"], fwd_ms=round(fm, 4), bwd_ms=round(bm, 4),
+                   ms=round(tot, 4), ms_std=round(float(np.std(np.add(f, b))), 4),
+                   tflops=round((g["flops_fwd"] + g["flops_bwd"]) / (tot * 1e-3) / 1e12, 2),
+                   fwd_tflops=round(g["flops_fwd"] / (fm * 1e-3) / 1e12, 2),
+                   bwd_tflops=round(g["flops_bwd"] / (bm * 1e-3) / 1e12, 2),
+                   tokens_per_s=round(g["tokens"] / (tot * 1e-3)),
+                   mfma_frac=round((g["flops_fwd"] + g["flops_bwd"]) / (tot * 1e-3) / 1e12
+                                   / BF16_PEAK_TFLOPS, 4),
+                   hbm_frac=round((fb + bb) / (tot * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
+        if "variant" in g:
+            rec["variant"] = g["variant"]
+        per_group.append(rec)
+        log(f"  {g['name']:>16s}  fwd {fm:8.3f} ms  bwd {bm:8.3f} ms  "
+            f"{rec['tflops']:8.1f} TFLOP/s  {rec['tokens_per_s'] / 1e6:8.2f} Mtok/s")
+
+    # Per-kernel durations from the library's event pairs (the kernel's stream).
+    kern = {}
+    for name, kid in _lib.KERNELS.items():
+        ms, n = _lib.prof_read(kid)
+        kern[name] = dict(total_ms=ms, launches=n, avg_ms=ms / n if n else 0.0)
+    per_pair = {"forward": 4, "backward_dkdv": 8, "backward_dq": 2}
+    alg = {name: sum(per_pair[name] * D * g["pairs"] for g in groups) * args.steps
+           for name in per_pair}
+    alg["backward_prep"] = sum(2 * g["tokens"] * H * D * 2 + g["tokens"] * H * 12
+                               for g in groups) * args.steps
+    dom = max(kern, key=lambda n: kern[n]["total_ms"])
+    kd = kern[dom]
+    launches = max(kd["launches"], 1)
+    if dom == "backward_prep":
+        achieved = alg[dom] / launches / (kd["avg_ms"] * 1e-3) / 1e9
+        roof = dict(bound="hbm", unit="GB/s", peak=HBM_PEAK_GBS)
+    else:
+        achieved = alg[dom] / launches / (kd["avg_ms"] * 1e-3) / 1e12
+        roof = dict(bound="mfma", unit="TFLOP/s", peak=BF16_PEAK_TFLOPS)
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            tr = json.load(f)
+        if tr.get("kernel") == dom and tr.get("workload") == desc["workload"]:
+            traffic = tr.get("bytes_per_launch")
+    roofline = dict(bound=roof["bound"], kernel=dom, achieved=round(achieved, 2),
+                    peak=roof["peak"], unit=roof["unit"], frac=round(achieved / roof["peak"], 4),
+                    traffic=traffic, launches=kd["launches"], avg_ms=round(kd["avg_ms"], 5),
+                    algorithmic_per_launch=alg[dom] // launches)
+    for name in kern:
+        kern[name]["avg_ms"] = round(kern[name]["avg_ms"], 5)
+        kern[name]["total_ms"] = round(kern[name]["total_ms"], 3)
+    log(f"dominant kernel {dom}: {roofline}")
+
+    result = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 on device; log-normal document lengths)",
+        "config": desc,
+        "tokens_per_s": round(tokens_step / (ms_per_step * 1e-3)),
+        "groups": per_group, "kernels": kern, "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(groups, desc, args)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(groups, desc, args):
+    """The fp64 oracle on a bounded sample: (b, h) pairs of one group."""
+    import numpy as np
+    import oracle
+    import synth
+
+    # The middle group of the workload, its sampled (b, h) pairs.
+    g = groups[len(groups) // 2]
+    B, L, H, D = g["B"], g["L"], g["H"], g["D"]
+    rng = np.random.default_rng(args.seed)
+    per_pair_flops = (g["flops_fwd"] + g["flops_bwd"]) / (B * H)
+    x = {n: synth.normal_bf16((B, L, H, D), args.seed, i + 1) for i, n in enumerate("qkv")}
+    x["do"] = synth.normal_bf16((B, L, H, D), args.seed, 4)
+
+    def run(pairs):
+        t = time.perf_counter()
+        oracle.attn_fwd(x["q"], x["k"], x["v"], causal=True, cu_doclens=g["cu"], bh=pairs)
+        oracle.attn_bwd(x["q"], x["k"], x["v"], x["do"], causal=True, cu_doclens=g["cu"],
+                        bh=pairs)
+        return time.perf_counter() - t
+
+    all_pairs = [(b, h) for b in range(B) for h in range(H)]
+    order = rng.permutation(len(all_pairs))
+    first = [all_pairs[order[0]]]
+    t1 = run(first)
+    n = int(min(len(all_pairs), max(1, args.cpu_seconds / max(t1, 1e-3))))
+    pairs = [all_pairs[i] for i in order[:n]]
+    secs = run(pairs) if n > 1 else t1
+    flops = per_pair_flops * n
+    log(f"cpu oracle: {n} (b,h) pairs of {g['name']} in {secs:.2f} s")
+    return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s",
+            "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"{g['name']} (B={B}, L={L}, H={H}, D={D}): fwd+bwd of {n} of the "
+                      f"{B * H} (b, h) pairs, fp64",
+            "seconds": round(secs, 3),
+            "tokens_per_s": round(n * L / secs, 1)}
+
+
+if __name__ == "__main__":
+    main()

@@ -34,8 +34,8 @@
  *
  * Ownership.  Every tensor pointer is a DEVICE pointer owned by the caller,
  * including the backward workspace.  The library allocates no device memory,
- * keeps no pointer after a call returns and holds no state, so calls are
- * thread-safe.  Work is enqueued asynchronously on `stream` (a hipStream_t;
+ * keeps no pointer after a call returns and, apart from the opt-in timing
+ * records of dd_prof_enable(), holds no state, so calls are thread-safe.  Work is enqueued asynchronously on `stream` (a hipStream_t;
  * NULL = the default stream); outputs are valid once the caller synchronises.
  *
  * Errors.  Arguments are validated on the host before anything is enqueued;
@@ -109,6 +109,26 @@ int dd_doclens_check(const int32_t *host_cu_doclens, int n_docs,
 
 /* Static English text of a status code ("unknown status" otherwise). */
 const char *dd_status_str(int status);
+
+/*
+ * Kernel timing (diagnostics; the method itself has no such step).
+ * While enabled, every kernel the library enqueues is bracketed by a pair of
+ * HIP events recorded on that kernel's own stream, so the elapsed time of
+ * each launch can be read back.  The events are created and owned by the
+ * library and reused across enable cycles.
+ *
+ * dd_prof_enable(1) discards earlier records and starts recording;
+ * dd_prof_enable(0) stops recording and keeps the records.
+ * dd_prof_read(kernel, &total_ms, &launches) waits for the recorded events
+ * of that kernel and returns the sum of their elapsed times and the number of
+ * launches; kernel ids are 0 forward, 1 backward preprocess (delta and
+ * log2-LSE), 2 backward dK/dV, 3 backward dQ.  Returns DD_OK, DD_ERR_NULL for
+ * a NULL output pointer, DD_ERR_SHAPE for an unknown kernel id, or
+ * DD_ERR_HIP if the runtime fails.  These calls are serialised internally.
+ */
+int dd_prof_enable(int on);
+int dd_prof_read(int kernel, double *total_ms, long long *launches);
+const char *dd_prof_kernel_name(int kernel); /* NULL for an unknown id */
 
 #ifdef __cplusplus
 }

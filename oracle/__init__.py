@@ -59,8 +59,15 @@ def _load():
             nout = 2 if "fwd" in name else 3
             fn.argtypes = [P] * nin + [I] * 5 + [P, I, P, I] + [P] * nout
             fn.restype = I
+        lib.oracle_threads.argtypes = []
+        lib.oracle_threads.restype = I
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """Threads the oracle's OpenMP loops use."""
+    return int(_load().oracle_threads())
 
 
 def _ptr(a):

@@ -338,3 +338,16 @@ int oracle_attn_bwd_f64(const double *q, const double *k, const double *v,
     return backward_any(1, q, k, v, dO, B, L, H, D, causal, cu_doclens, n_docs,
                         bh, n_bh, dq, dk, dv);
 }
+
+/* Number of threads the OpenMP loops above run with. */
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+int oracle_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

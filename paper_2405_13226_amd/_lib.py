@@ -20,7 +20,24 @@ SIGNATURES = {
     "dd_attn_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I]),
     "dd_doclens_check": (ctypes.c_int, [_P, _I, ctypes.c_longlong]),
     "dd_status_str": (ctypes.c_char_p, [_I]),
+    "dd_prof_enable": (ctypes.c_int, [_I]),
+    "dd_prof_read": (ctypes.c_int, [_I, ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(ctypes.c_longlong)]),
+    "dd_prof_kernel_name": (ctypes.c_char_p, [_I]),
 }
+
+KERNELS = {"forward": 0, "backward_prep": 1, "backward_dkdv": 2, "backward_dq": 3}
+
+
+def prof_enable(on: bool) -> None:
+    check(lib().dd_prof_enable(int(bool(on))), "dd_prof_enable")
+
+
+def prof_read(kernel: int):
+    """(total ms, launches) of one kernel since the last prof_enable(True)."""
+    ms, n = ctypes.c_double(0.0), ctypes.c_longlong(0)
+    check(lib().dd_prof_read(int(kernel), ctypes.byref(ms), ctypes.byref(n)), "dd_prof_read")
+    return ms.value, n.value
 
 STATUS = {
     0: "DD_OK", 1: "DD_ERR_NULL", 2: "DD_ERR_SHAPE", 3: "DD_ERR_HEADDIM",

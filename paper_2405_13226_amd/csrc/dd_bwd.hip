@@ -22,6 +22,7 @@
 #include "dd_device.hpp"
 #include "dd_internal.h"
 #include "dd_launch.hpp"
+#include "dd_prof.hpp"
 #include "dd_attn.h"
 
 namespace dd {
@@ -506,22 +507,32 @@ static int launch_bwd_d(const BwdArgs &a)
 
     const long long threads = static_cast<long long>(a.B) * a.L * a.H * (D / 8);
     const unsigned pblocks = static_cast<unsigned>((threads + 255) / 256);
-    hipError_t e = launch_kernel(prep_kernel<D>, dim3(pblocks), dim3(256), st, a.O, a.dO, a.LSE,
-                                 lse2, delta, a.B, a.L, a.H);
+    hipError_t e;
+    {
+        ProfScope prof(K_PREP, st);
+        e = launch_kernel(prep_kernel<D>, dim3(pblocks), dim3(256), st, a.O, a.dO, a.LSE, lse2,
+                          delta, a.B, a.L, a.H);
+    }
     if (e != hipSuccess)
         return DD_ERR_HIP;
 
     const int nkb = (a.L + KvTile<D>::BN - 1) / KvTile<D>::BN;
-    e = launch_kernel(dkdv_kernel<D>, dim3(static_cast<unsigned>(nkb * a.B * a.H)), dim3(256), st,
-                      a.Q, a.K, a.V, a.dO, lse2, delta, a.dK, a.dV, a.B, a.L, a.H,
-                      a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, scale, nkb);
+    {
+        ProfScope prof(K_DKDV, st);
+        e = launch_kernel(dkdv_kernel<D>, dim3(static_cast<unsigned>(nkb * a.B * a.H)), dim3(256),
+                          st, a.Q, a.K, a.V, a.dO, lse2, delta, a.dK, a.dV, a.B, a.L, a.H,
+                          a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, scale, nkb);
+    }
     if (e != hipSuccess)
         return DD_ERR_HIP;
 
     const int nqb = (a.L + QTile<D>::BM - 1) / QTile<D>::BM;
-    e = launch_kernel(dq_kernel<D>, dim3(static_cast<unsigned>(nqb * a.B * a.H)), dim3(256), st,
-                      a.Q, a.K, a.V, a.dO, lse2, delta, a.dQ, a.B, a.L, a.H, a.causal ? 1 : 0,
-                      a.cu, a.n_docs, scale_log2, scale, nqb);
+    {
+        ProfScope prof(K_DQ, st);
+        e = launch_kernel(dq_kernel<D>, dim3(static_cast<unsigned>(nqb * a.B * a.H)), dim3(256),
+                          st, a.Q, a.K, a.V, a.dO, lse2, delta, a.dQ, a.B, a.L, a.H,
+                          a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, scale, nqb);
+    }
     return e == hipSuccess ? DD_OK : DD_ERR_HIP;
 }
 

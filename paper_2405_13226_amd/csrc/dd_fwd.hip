@@ -18,6 +18,7 @@
 #include "dd_device.hpp"
 #include "dd_internal.h"
 #include "dd_launch.hpp"
+#include "dd_prof.hpp"
 #include "dd_attn.h"
 
 namespace dd {
@@ -242,6 +243,7 @@ static int launch_fwd_d(const FwdArgs &a)
     const int nqb = (a.L + FwdTile<D>::BM - 1) / FwdTile<D>::BM;
     const long long blocks = static_cast<long long>(nqb) * a.B * a.H;
     const float scale_log2 = kLog2e / sqrtf(static_cast<float>(D));
+    ProfScope prof(K_FWD, static_cast<hipStream_t>(a.stream));
     const hipError_t e = launch_kernel(
         fwd_kernel<D>, dim3(static_cast<unsigned>(blocks)), dim3(256),
         static_cast<hipStream_t>(a.stream), a.Q, a.K, a.V, a.O, a.LSE, a.B, a.L, a.H,
