@@ -10,16 +10,17 @@
 //               S = Q K^T, P = exp2(S*scale*log2e - lse2), dP = dO V^T,
 //               dS = P * (dP - delta),
 //               dV^T += dO^T P,  dK^T += Q^T dS.
-//             Q and dO tiles are staged in LDS both row-major (operands of S
-//             and dP) and transposed (operands of dV^T and dK^T).
+//             Q and dO tiles arrive row-major in LDS by direct DMA; S and dP
+//             read them row-wise, dV^T and dK^T transposed (ds_read_b64_tr_b16).
 //   3. dq:    query-resident.  One workgroup = 4 waves = 128 queries; each
 //             wave keeps its queries' Q and dO rows in registers, walks the
 //             key tiles (64 keys) its queries see and forms
 //               S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T,
-//             with K (row-major and transposed) and V tiles in LDS.
+//             with K and V tiles in LDS (K^T read transposed).
 // Splitting dQ from dK/dV keeps every output owned by exactly one workgroup:
 // no atomics, deterministic results, at the cost of recomputing S and dP.
 #include "dd_device.hpp"
+#include "dd_tile.hpp"
 #include "dd_internal.h"
 #include "dd_launch.hpp"
 #include "dd_prof.hpp"
@@ -67,19 +68,18 @@ prep_kernel(const uint16_t *__restrict__ O, const uint16_t *__restrict__ dO,
 // ---------------------------------------------------------------------------
 // 2. dK, dV
 // ---------------------------------------------------------------------------
+template <int N>
+struct IC {
+    static constexpr int value = N;
+};
+
 template <int D>
 struct KvTile {
-    static constexpr int BN = 128;     // keys per workgroup
-    static constexpr int BM = 64;      // queries per tile
-    static constexpr int RP = D + 8;   // row-major pitch
-    static constexpr int TP = BM + 4;  // transposed pitch
-    static constexpr int R_ELEMS = BM * RP;
-    static constexpr int T_ELEMS = D * TP;
-    // Q rows, dO rows, Q^T, dO^T, then lse2[BM] and delta[BM] as floats.
-    static constexpr int STAGE = 2 * R_ELEMS + 2 * T_ELEMS + 2 * BM * 2;
-    static constexpr int UNITS = 2 * (BM / 4) * (D / 8);
-    static constexpr int UNITS_PER_THREAD = UNITS / 256;
-    static_assert(UNITS % 256 == 0, "tile units must divide the workgroup");
+    static constexpr int BN = 128;            // keys per workgroup
+    static constexpr int BM = 64;             // queries per tile
+    static constexpr int TILE = BM * D;       // elements of a Q or dO tile
+    // Q tile, dO tile, then lse2[BM] and delta[BM] as floats.
+    static constexpr int STAGE = 2 * TILE + 2 * BM * 2;
 };
 
 template <int D>
@@ -94,7 +94,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     using T = KvTile<D>;
     constexpr int KK = D / 16;
     constexpr int DB = D / 32;
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2 * T::STAGE];
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE];
 
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
@@ -145,6 +145,22 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         vf[kk] = as_bf16x8(vv);
     }
 
+    // Per-lane LDS offsets: row reads (row l32 of a 32-query block, chunk
+    // 2*kk + g) and transposed reads (rows 8*hh + 4*g + e of a 16-query step,
+    // columns db*32 + 16*(G&1) + 4*c), shared by the Q and dO tiles.
+    int roff[KK], toff[DB][2];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+        roff[kk] = tile_off<D>(l32, kk * 16 + g * 8);
+    {
+        const int G = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G & 1) + 4 * c);
+    }
+
     f32x16 dk[DB], dv[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
@@ -152,133 +168,115 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         dv[db] = f32x16{};
     }
 
-    Unit4x8 pre[T::UNITS_PER_THREAD];
-    float pre_f = 0.f;
-    auto issue_loads = [&](int t) {
+    DmaPlan<D, T::BM, 4> plan;
+    plan.init(rs, wave, lane);
+    auto issue = [&](int t, uint16_t *stage) {
         const int i0 = t * T::BM;
-#pragma unroll
-        for (int i = 0; i < T::UNITS_PER_THREAD; ++i) {
-            const int u = tid + 256 * i;
-            if (u < T::UNITS / 2)
-                load_unit<D>(pre[i], Qb, rs, i0, L, u);
-            else
-                load_unit<D>(pre[i], dOb, rs, i0, L, u - T::UNITS / 2);
-        }
-        if (tid < 2 * T::BM) {
-            const int q = i0 + (tid % T::BM);
-            pre_f = q < L ? (tid < T::BM ? lse2[q] : dlt[q]) : 0.f;
-        }
-    };
-    auto commit = [&](int buf) {
-        uint16_t *qs = lds + buf * T::STAGE;
-        uint16_t *dos = qs + T::R_ELEMS;
-        uint16_t *qt = dos + T::R_ELEMS;
-        uint16_t *dot = qt + T::T_ELEMS;
-        float *fs = reinterpret_cast<float *>(dot + T::T_ELEMS);
-#pragma unroll
-        for (int i = 0; i < T::UNITS_PER_THREAD; ++i) {
-            const int u = tid + 256 * i;
-            if (u < T::UNITS / 2) {
-                store_unit_rows<D, T::RP>(pre[i], qs, u);
-                store_unit_cols<D, T::TP>(pre[i], qt, u);
-            } else {
-                store_unit_rows<D, T::RP>(pre[i], dos, u - T::UNITS / 2);
-                store_unit_cols<D, T::TP>(pre[i], dot, u - T::UNITS / 2);
-            }
-        }
-        if (tid < 2 * T::BM)
-            fs[tid] = pre_f;
+        plan.issue(stage, Qb, rs, i0, L, wave, lane);
+        plan.issue(stage + T::TILE, dOb, rs, i0, L, wave, lane);
+        float *fs = reinterpret_cast<float *>(stage + 2 * T::TILE);
+        if (wave == 0)
+            dma_row_f32(fs, lse2, i0, L, lane);
+        else if (wave == 1)
+            dma_row_f32(fs + T::BM, dlt, i0, L, lane);
     };
 
-    issue_loads(t_begin);
-    commit(0);
+    auto compute = [&](int t, auto bufc) {
+        constexpr int BUF = decltype(bufc)::value;
+        const uint16_t *qs = lds + BUF * T::STAGE;
+        const uint16_t *dos = qs + T::TILE;
+        const float *lse_s = reinterpret_cast<const float *>(qs + 2 * T::TILE);
+        const float *dlt_s = lse_s + T::BM;
+        const int i0 = t * T::BM;
+        if (!(wave_on && i0 <= hi_w && i0 + T::BM - 1 >= lo_w))
+            return;
+        const bool full = wave_full_keys && i0 >= lo_all && i0 + T::BM - 1 <= hi_all;
+
+        // S = Q K^T and dP = dO V^T for two 32-query blocks
+        // (C layout: column = this lane's key, rows = queries).
+        f32x16 s[2], dp[2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            s[qb] = f32x16{};
+            dp[qb] = f32x16{};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const int off = qb * 32 * D + roff[kk];
+                s[qb] = mfma32(lds_row8(qs + off), kf[kk], s[qb]);
+                dp[qb] = mfma32(lds_row8(dos + off), vf[kk], dp[qb]);
+            }
+        }
+
+        // P = exp2(S*c - lse2) and dS = P (dP - delta), in place.
+        const int qlo_r = qlo_k - i0 - 4 * g, qhi_r = qhi_k - i0 - 4 * g;
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+                const int ql = qb * 32 + 8 * rg + 4 * g;
+                const f32x4 lz = *reinterpret_cast<const f32x4 *>(lse_s + ql);
+                const f32x4 dz = *reinterpret_cast<const f32x4 *>(dlt_s + ql);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int r = 4 * rg + e;
+                    float p = fast_exp2(fmaf(s[qb][r], scale_log2, -lz[e]));
+                    if (!full) {
+                        const int qr = qb * 32 + 8 * rg + e;
+                        const bool ok = (qr >= qlo_r) & (qr <= qhi_r);
+                        p = ok ? p : 0.f;
+                    }
+                    s[qb][r] = p;
+                    dp[qb][r] = p * (dp[qb][r] - dz[e]);
+                }
+            }
+
+        // dV^T += dO^T P and dK^T += Q^T dS.  B operand (qb, t2): rows
+        // 8*t2..8*t2+7 of the C layout = queries qb*32+16*t2+4g+{0..3}, +8;
+        // the A operands read exactly those queries transposed.
+        bf16x8 pb[2][2], sb[2][2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2) {
+                pb[qb][t2] = pack8(s[qb], 8 * t2);
+                sb[qb][t2] = pack8(dp[qb], 8 * t2);
+            }
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const int ro = (qb * 32 + 16 * t2) * D;
+                    const bf16x8 ado = join(lds_tr4(dos + ro + toff[db][0]),
+                                            lds_tr4(dos + ro + toff[db][1]));
+                    const bf16x8 aq = join(lds_tr4(qs + ro + toff[db][0]),
+                                           lds_tr4(qs + ro + toff[db][1]));
+                    dv[db] = mfma32(ado, pb[qb][t2], dv[db]);
+                    dk[db] = mfma32(aq, sb[qb][t2], dk[db]);
+                }
+    };
+
+    issue(t_begin, lds);
+    wait_vmem();
     __syncthreads();
-
-    int buf = 0;
-    for (int t = t_begin; t <= t_end; ++t) {
+    for (int t = t_begin;;) {
         if (t < t_end)
-            issue_loads(t + 1);
-
-        const int i0 = t * T::BM;
-        const bool active = wave_on && i0 <= hi_w && i0 + T::BM - 1 >= lo_w;
-        if (active) {
-            const uint16_t *qs = lds + buf * T::STAGE;
-            const uint16_t *dos = qs + T::R_ELEMS;
-            const uint16_t *qt = dos + T::R_ELEMS;
-            const uint16_t *dot = qt + T::T_ELEMS;
-            const float *lse_s = reinterpret_cast<const float *>(dot + T::T_ELEMS);
-            const float *dlt_s = lse_s + T::BM;
-            const bool full = wave_full_keys && i0 >= lo_all && i0 + T::BM - 1 <= hi_all;
-
-            // S = Q K^T and dP = dO V^T for two 32-query blocks
-            // (C layout: column = this lane's key, rows = queries).
-            f32x16 s[2], dp[2];
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) {
-                s[qb] = f32x16{};
-                dp[qb] = f32x16{};
-#pragma unroll
-                for (int kk = 0; kk < KK; ++kk) {
-                    const int off = (qb * 32 + l32) * T::RP + kk * 16 + g * 8;
-                    const bf16x8 aq = as_bf16x8(*reinterpret_cast<const u32x4 *>(qs + off));
-                    const bf16x8 ad = as_bf16x8(*reinterpret_cast<const u32x4 *>(dos + off));
-                    s[qb] = mfma32(aq, kf[kk], s[qb]);
-                    dp[qb] = mfma32(ad, vf[kk], dp[qb]);
-                }
-            }
-
-            // P and dS in place (s <- P, dp <- dS).
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-                for (int rg = 0; rg < 4; ++rg) {
-                    const int ql = qb * 32 + 8 * rg + 4 * g;
-                    const f32x4 lz = *reinterpret_cast<const f32x4 *>(lse_s + ql);
-                    const f32x4 dz = *reinterpret_cast<const f32x4 *>(dlt_s + ql);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int r = 4 * rg + e;
-                        float p = fast_exp2(s[qb][r] * scale_log2 - lz[e]);
-                        if (!full) {
-                            const int q = i0 + ql + e;
-                            if (q < qlo_k || q > qhi_k)
-                                p = 0.f;
-                        }
-                        s[qb][r] = p;
-                        dp[qb][r] = p * (dp[qb][r] - dz[e]);
-                    }
-                }
-
-            // dV^T += dO^T P and dK^T += Q^T dS.  B operand (qb, t2): rows
-            // 8*t2..8*t2+7 of the C layout = queries qb*32+16*t2+4g+{0..3}, +8.
-            bf16x8 pb[2][2], sb[2][2];
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-                for (int t2 = 0; t2 < 2; ++t2) {
-                    pb[qb][t2] = pack8(s[qb], 8 * t2);
-                    sb[qb][t2] = pack8(dp[qb], 8 * t2);
-                }
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-                    for (int t2 = 0; t2 < 2; ++t2) {
-                        const int off = (db * 32 + l32) * T::TP + qb * 32 + 16 * t2 + 4 * g;
-                        const bf16x8 ado = join(*reinterpret_cast<const bf16x4 *>(dot + off),
-                                                *reinterpret_cast<const bf16x4 *>(dot + off + 8));
-                        const bf16x8 aqt = join(*reinterpret_cast<const bf16x4 *>(qt + off),
-                                                *reinterpret_cast<const bf16x4 *>(qt + off + 8));
-                        dv[db] = mfma32(ado, pb[qb][t2], dv[db]);
-                        dk[db] = mfma32(aqt, sb[qb][t2], dk[db]);
-                    }
-        }
-
-        if (t < t_end)
-            commit(buf ^ 1);
+            issue(t + 1, lds + T::STAGE);
+        compute(t, IC<0>{});
+        wait_vmem();
         __syncthreads();
-        buf ^= 1;
+        if (t == t_end)
+            break;
+        ++t;
+        if (t < t_end)
+            issue(t + 1, lds);
+        compute(t, IC<1>{});
+        wait_vmem();
+        __syncthreads();
+        if (t == t_end)
+            break;
+        ++t;
     }
 
     if (!k_ok)
@@ -303,21 +301,14 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 // ---------------------------------------------------------------------------
 template <int D>
 struct QTile {
-    static constexpr int BM = 128;     // queries per workgroup
-    static constexpr int BN = 64;      // keys per tile
-    static constexpr int RP = D + 8;
-    static constexpr int TP = BN + 4;
-    static constexpr int R_ELEMS = BN * RP;
-    static constexpr int T_ELEMS = D * TP;
-    // K rows, V rows, K^T.
-    static constexpr int STAGE = 2 * R_ELEMS + T_ELEMS;
-    static constexpr int UNITS = 2 * (BN / 4) * (D / 8);
-    static constexpr int UNITS_PER_THREAD = UNITS / 256;
-    static_assert(UNITS % 256 == 0, "tile units must divide the workgroup");
+    static constexpr int BM = 128;         // queries per workgroup
+    static constexpr int BN = 64;          // keys per tile
+    static constexpr int TILE = BN * D;    // elements of a K or V tile
+    static constexpr int STAGE = 2 * TILE; // K then V
 };
 
 template <int D>
-__global__ void __launch_bounds__(256, 1)
+__global__ void __launch_bounds__(256, 2)
 dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
           const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
           const float *__restrict__ lse2g, const float *__restrict__ deltag,
@@ -327,7 +318,7 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     using T = QTile<D>;
     constexpr int KK = D / 16;
     constexpr int DB = D / 32;
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2 * T::STAGE];
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE];
 
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
@@ -373,111 +364,109 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         dof[kk] = as_bf16x8(dv);
     }
     const long long wrow = static_cast<long long>(bh) * L;
-    const float my_lse2 = q_ok ? lse2g[wrow + my_q] : 0.f;
+    const float neg_lse2 = q_ok ? -lse2g[wrow + my_q] : 0.f;
     const float my_delta = q_ok ? deltag[wrow + my_q] : 0.f;
+
+    int roff[KK], toff[DB][2];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+        roff[kk] = tile_off<D>(l32, kk * 16 + g * 8);
+    {
+        const int G = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G & 1) + 4 * c);
+    }
 
     f32x16 dq[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db)
         dq[db] = f32x16{};
 
-    Unit4x8 pre[T::UNITS_PER_THREAD];
-    auto issue_loads = [&](int t) {
-        const int j0 = t * T::BN;
-#pragma unroll
-        for (int i = 0; i < T::UNITS_PER_THREAD; ++i) {
-            const int u = tid + 256 * i;
-            if (u < T::UNITS / 2)
-                load_unit<D>(pre[i], Kb, rs, j0, L, u);
-            else
-                load_unit<D>(pre[i], Vb, rs, j0, L, u - T::UNITS / 2);
-        }
-    };
-    auto commit = [&](int buf) {
-        uint16_t *ks = lds + buf * T::STAGE;
-        uint16_t *vs = ks + T::R_ELEMS;
-        uint16_t *kt = vs + T::R_ELEMS;
-#pragma unroll
-        for (int i = 0; i < T::UNITS_PER_THREAD; ++i) {
-            const int u = tid + 256 * i;
-            if (u < T::UNITS / 2) {
-                store_unit_rows<D, T::RP>(pre[i], ks, u);
-                store_unit_cols<D, T::TP>(pre[i], kt, u);
-            } else {
-                store_unit_rows<D, T::RP>(pre[i], vs, u - T::UNITS / 2);
-            }
-        }
+    DmaPlan<D, T::BN, 4> plan;
+    plan.init(rs, wave, lane);
+    auto issue = [&](int t, uint16_t *stage) {
+        plan.issue(stage, Kb, rs, t * T::BN, L, wave, lane);
+        plan.issue(stage + T::TILE, Vb, rs, t * T::BN, L, wave, lane);
     };
 
-    issue_loads(t_begin);
-    commit(0);
+    auto compute = [&](int t, auto bufc) {
+        constexpr int BUF = decltype(bufc)::value;
+        const uint16_t *ks = lds + BUF * T::STAGE;
+        const uint16_t *vs = ks + T::TILE;
+        const int j0 = t * T::BN;
+        if (!(wave_on && j0 <= hi_w && j0 + T::BN - 1 >= lo_w))
+            return;
+        const bool full = wave_full_rows && j0 >= lo_all && j0 + T::BN - 1 <= hi_all;
+
+        // S^T = K Q^T and dP^T = V dO^T (column = this lane's query).
+        f32x16 s[2], dp[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            s[kb] = f32x16{};
+            dp[kb] = f32x16{};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const int off = kb * 32 * D + roff[kk];
+                s[kb] = mfma32(lds_row8(ks + off), qf[kk], s[kb]);
+                dp[kb] = mfma32(lds_row8(vs + off), dof[kk], dp[kb]);
+            }
+        }
+        const int lo_r = lo_q - j0 - 4 * g, hi_r = hi_q - j0 - 4 * g;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float p = fast_exp2(fmaf(s[kb][r], scale_log2, neg_lse2));
+                if (!full) {
+                    const int kr = kb * 32 + 8 * (r >> 2) + (r & 3);
+                    const bool ok = (kr >= lo_r) & (kr <= hi_r);
+                    p = ok ? p : 0.f;
+                }
+                dp[kb][r] = p * (dp[kb][r] - my_delta);
+            }
+
+        // dQ^T += K^T dS^T, K^T read transposed from the K tile.
+        bf16x8 sb[2][2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2)
+                sb[kb][t2] = pack8(dp[kb], 8 * t2);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const uint16_t *kr = ks + (kb * 32 + 16 * t2) * D;
+                    const bf16x8 a = join(lds_tr4(kr + toff[db][0]), lds_tr4(kr + toff[db][1]));
+                    dq[db] = mfma32(a, sb[kb][t2], dq[db]);
+                }
+    };
+
+    issue(t_begin, lds);
+    wait_vmem();
     __syncthreads();
-
-    int buf = 0;
-    for (int t = t_begin; t <= t_end; ++t) {
+    for (int t = t_begin;;) {
         if (t < t_end)
-            issue_loads(t + 1);
-
-        const int j0 = t * T::BN;
-        const bool active = wave_on && j0 <= hi_w && j0 + T::BN - 1 >= lo_w;
-        if (active) {
-            const uint16_t *ks = lds + buf * T::STAGE;
-            const uint16_t *vs = ks + T::R_ELEMS;
-            const uint16_t *kt = vs + T::R_ELEMS;
-            const bool full = wave_full_rows && j0 >= lo_all && j0 + T::BN - 1 <= hi_all;
-
-            // S^T = K Q^T and dP^T = V dO^T (column = this lane's query).
-            f32x16 s[2], dp[2];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                s[kb] = f32x16{};
-                dp[kb] = f32x16{};
-#pragma unroll
-                for (int kk = 0; kk < KK; ++kk) {
-                    const int off = (kb * 32 + l32) * T::RP + kk * 16 + g * 8;
-                    const bf16x8 ak = as_bf16x8(*reinterpret_cast<const u32x4 *>(ks + off));
-                    const bf16x8 av = as_bf16x8(*reinterpret_cast<const u32x4 *>(vs + off));
-                    s[kb] = mfma32(ak, qf[kk], s[kb]);
-                    dp[kb] = mfma32(av, dof[kk], dp[kb]);
-                }
-            }
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    float p = fast_exp2(s[kb][r] * scale_log2 - my_lse2);
-                    if (!full) {
-                        const int key = j0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-                        if (key < lo_q || key > hi_q)
-                            p = 0.f;
-                    }
-                    dp[kb][r] = p * (dp[kb][r] - my_delta);
-                }
-
-            // dQ^T += K^T dS^T.
-            bf16x8 sb[2][2];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int t2 = 0; t2 < 2; ++t2)
-                    sb[kb][t2] = pack8(dp[kb], 8 * t2);
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int t2 = 0; t2 < 2; ++t2) {
-                        const int off = (db * 32 + l32) * T::TP + kb * 32 + 16 * t2 + 4 * g;
-                        const bf16x8 a = join(*reinterpret_cast<const bf16x4 *>(kt + off),
-                                              *reinterpret_cast<const bf16x4 *>(kt + off + 8));
-                        dq[db] = mfma32(a, sb[kb][t2], dq[db]);
-                    }
-        }
-
-        if (t < t_end)
-            commit(buf ^ 1);
+            issue(t + 1, lds + T::STAGE);
+        compute(t, IC<0>{});
+        wait_vmem();
         __syncthreads();
-        buf ^= 1;
+        if (t == t_end)
+            break;
+        ++t;
+        if (t < t_end)
+            issue(t + 1, lds);
+        compute(t, IC<1>{});
+        wait_vmem();
+        __syncthreads();
+        if (t == t_end)
+            break;
+        ++t;
     }
 
     if (!q_ok)
@@ -493,6 +482,28 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                       dq[db][4 * rg + 2] * scale, dq[db][4 * rg + 3] * scale);
         }
 }
+
+// Explicit instantiations: the host-side launch stubs of these kernel
+// templates are emitted here unconditionally (clang's host pass does not
+// always emit them for templates only referenced through a function pointer).
+#define DD_BWD_INSTANTIATE(D)                                                                    \
+    template __global__ void prep_kernel<D>(const uint16_t *__restrict__,                       \
+                                            const uint16_t *__restrict__,                       \
+                                            const float *__restrict__, float *__restrict__,     \
+                                            float *__restrict__, int, int, int);                \
+    template __global__ void dkdv_kernel<D>(                                                     \
+        const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__, \
+        const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,      \
+        uint16_t *__restrict__, uint16_t *__restrict__, int, int, int, int,                      \
+        const int32_t *__restrict__, int, float, float, int);                                    \
+    template __global__ void dq_kernel<D>(                                                       \
+        const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__, \
+        const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,      \
+        uint16_t *__restrict__, int, int, int, int, const int32_t *__restrict__, int, float,     \
+        float, int);
+DD_BWD_INSTANTIATE(64)
+DD_BWD_INSTANTIATE(128)
+#undef DD_BWD_INSTANTIATE
 
 // ---------------------------------------------------------------------------
 template <int D>

@@ -4,18 +4,20 @@
 // One workgroup = 4 waves = BM = 128 queries of one (b, h) slice; each wave
 // owns 32 queries and keeps their Q rows in registers as matrix-core B
 // operands.  The workgroup walks the key tiles (BN = 64 keys) that the mask
-// allows for its queries; K (row-major) and V (transposed) tiles are staged
-// in LDS, double-buffered, with the next tile's global loads in flight while
-// the current one is consumed.
+// allows for its queries.  K and V tiles arrive in LDS by direct
+// global->LDS DMA (row-major, XOR-swizzled), double-buffered: the next tile's
+// loads are in flight while the current one is consumed.
 //
 // Per wave and tile the product is computed transposed: S^T = K Q^T puts one
 // query per lane column, so the softmax row max/sum is an in-lane reduction
 // plus one exchange with lane l^32, and P^T stays in registers as the B
-// operand of O^T += V^T P^T.  The online softmax keeps a running max m and
+// operand of O^T += V^T P^T, whose A operand is read transposed from the
+// row-major V tile (ds_read_b64_tr_b16).  The online softmax keeps a running max m and
 // sum l in fp32 (log2 domain), rescaling the O accumulator when m grows.
 // Key tiles entirely outside the mask are never visited; tiles entirely
 // inside it skip the element mask (only boundary tiles evaluate it).
 #include "dd_device.hpp"
+#include "dd_tile.hpp"
 #include "dd_internal.h"
 #include "dd_launch.hpp"
 #include "dd_prof.hpp"
@@ -23,19 +25,24 @@
 
 namespace dd {
 
+template <int N>
+struct IC {
+    static constexpr int value = N;
+};
+
 template <int D>
 struct FwdTile {
-    static constexpr int BM = 128;       // queries per workgroup
-    static constexpr int BN = 64;        // keys per tile
-    static constexpr int KP = D + 8;     // K tile row pitch (elements)
-    static constexpr int VP = BN + 4;    // V^T tile row pitch (elements)
-    static constexpr int K_ELEMS = BN * KP;
-    static constexpr int V_ELEMS = D * VP;
-    static constexpr int STAGE = K_ELEMS + V_ELEMS;
-    static constexpr int UNITS = 2 * (BN / 4) * (D / 8);  // K and V units per tile
-    static constexpr int UNITS_PER_THREAD = UNITS / 256;
-    static_assert(UNITS % 256 == 0, "tile units must divide the workgroup");
+    static constexpr int BM = 128;            // queries per workgroup
+    static constexpr int BN = 64;             // keys per tile
+    static constexpr int TILE = BN * D;       // elements of one K or V tile
+    static constexpr int STAGE = 2 * TILE;    // K then V
 };
+
+// Rescaling of the output accumulator is skipped until the running maximum
+// has grown by more than this many log2 units; probabilities then stay below
+// 2^8, and the final normalisation uses the same reference, so the result is
+// unchanged.
+constexpr float kRescaleSlack = 8.0f;
 
 template <int D>
 __global__ void __launch_bounds__(256, 2)
@@ -47,7 +54,7 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     using T = FwdTile<D>;
     constexpr int KK = D / 16;  // k-steps of S^T
     constexpr int DB = D / 32;  // 32-row blocks of O^T
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2 * T::STAGE];
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE];
 
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
@@ -72,12 +79,11 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     if (q_ok)
         query_keys(b, L, my_q, causal, cu, n_docs, lo_q, hi_q);
     const bool wave_on = q0w < L;
-    // Wave key range and the sub-range every query of the wave allows.
     const int lo_w = wave_min(q_ok ? lo_q : 0x7fffffff);
     const int hi_w = wave_max(q_ok ? hi_q : -1);
     const int lo_all = wave_max(q_ok ? lo_q : -1);
     const int hi_all = wave_min(q_ok ? hi_q : 0x7fffffff);
-    const bool wave_full_rows = (q0w + 31) < L;  // no padding rows in the wave
+    const bool wave_full_rows = (q0w + 31) < L;
 
     // Workgroup key range: union over its queries (monotone in the query).
     const int qf = qb * T::BM, ql = min(qb * T::BM + T::BM - 1, L - 1);
@@ -96,127 +102,139 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         qf8[kk] = as_bf16x8(v);
     }
 
+    // Per-lane LDS offsets (elements, relative to a tile).  K row reads: row
+    // l32 of a 32-key block, chunk 2*kk + g.  V transposed reads: rows
+    // 8*hh + 4*g + e of a 16-key step, columns db*32 + 16*(G&1) + 4*c.
+    int koff[KK], voff[DB][2];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+        koff[kk] = tile_off<D>(l32, kk * 16 + g * 8);
+    {
+        const int G = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+                voff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G & 1) + 4 * c);
+    }
+
     f32x16 acc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db)
         acc[db] = f32x16{};
     float m_i = -INFINITY, l_i = 0.f;
 
-    // Stage the first tile.
-    Unit4x8 pre[T::UNITS_PER_THREAD];
-    auto issue_loads = [&](int t) {
-        const int j0 = t * T::BN;
-#pragma unroll
-        for (int i = 0; i < T::UNITS_PER_THREAD; ++i) {
-            const int u = tid + 256 * i;
-            if (u < T::UNITS / 2)
-                load_unit<D>(pre[i], Kb, rs, j0, L, u);
-            else
-                load_unit<D>(pre[i], Vb, rs, j0, L, u - T::UNITS / 2);
-        }
-    };
-    auto commit = [&](int buf) {
-        uint16_t *ks = lds + buf * T::STAGE;
-        uint16_t *vt = ks + T::K_ELEMS;
-#pragma unroll
-        for (int i = 0; i < T::UNITS_PER_THREAD; ++i) {
-            const int u = tid + 256 * i;
-            if (u < T::UNITS / 2)
-                store_unit_rows<D, T::KP>(pre[i], ks, u);
-            else
-                store_unit_cols<D, T::VP>(pre[i], vt, u - T::UNITS / 2);
-        }
+    DmaPlan<D, T::BN, 4> plan;
+    plan.init(rs, wave, lane);
+    auto issue = [&](int t, uint16_t *stage) {
+        plan.issue(stage, Kb, rs, t * T::BN, L, wave, lane);
+        plan.issue(stage + T::TILE, Vb, rs, t * T::BN, L, wave, lane);
     };
 
-    issue_loads(t_begin);
-    commit(0);
-    __syncthreads();
-
-    int buf = 0;
-    for (int t = t_begin; t <= t_end; ++t) {
-        if (t < t_end)
-            issue_loads(t + 1);
-
+    auto compute = [&](int t, auto bufc) {
+        constexpr int BUF = decltype(bufc)::value;
+        const uint16_t *kt = lds + BUF * T::STAGE;
+        const uint16_t *vt = kt + T::TILE;
         const int j0 = t * T::BN;
-        const bool active = wave_on && j0 <= hi_w && j0 + T::BN - 1 >= lo_w;
-        if (active) {
-            const uint16_t *ks = lds + buf * T::STAGE;
-            const uint16_t *vt = ks + T::K_ELEMS;
-            const bool full = wave_full_rows && j0 >= lo_all && j0 + T::BN - 1 <= hi_all;
+        if (!(wave_on && j0 <= hi_w && j0 + T::BN - 1 >= lo_w))
+            return;
+        const bool full = wave_full_rows && j0 >= lo_all && j0 + T::BN - 1 <= hi_all;
 
-            // S^T = K Q^T for two 32-key blocks.
-            f32x16 s[2];
+        // S^T = K Q^T for two 32-key blocks.
+        f32x16 s[2];
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                s[kb] = f32x16{};
+        for (int kb = 0; kb < 2; ++kb) {
+            s[kb] = f32x16{};
 #pragma unroll
-                for (int kk = 0; kk < KK; ++kk) {
-                    const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4 *>(
-                        ks + (kb * 32 + l32) * T::KP + kk * 16 + g * 8));
-                    s[kb] = mfma32(a, qf8[kk], s[kb]);
-                }
-            }
+            for (int kk = 0; kk < KK; ++kk)
+                s[kb] = mfma32(lds_row8(kt + kb * 32 * D + koff[kk]), qf8[kk], s[kb]);
+        }
 
-            // Scale into the log2 domain, mask boundary tiles, tile max.
-            float mt = -INFINITY;
+        // Boundary tiles: keys outside [lo_q, hi_q] -> -inf (branch-free).
+        if (!full) {
+            const int lo_r = lo_q - j0 - 4 * g, hi_r = hi_q - j0 - 4 * g;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    float x = s[kb][r] * scale_log2;
-                    if (!full) {
-                        const int key = j0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-                        if (key < lo_q || key > hi_q)
-                            x = -INFINITY;
-                    }
-                    s[kb][r] = x;
-                    mt = fmaxf(mt, x);
+                    const int kr = kb * 32 + 8 * (r >> 2) + (r & 3);
+                    const bool ok = (kr >= lo_r) & (kr <= hi_r);
+                    s[kb][r] = ok ? s[kb][r] : -INFINITY;
                 }
-            mt = fmaxf(mt, __shfl_xor(mt, 32));
-            const float m_new = fmaxf(m_i, mt);
-            const float m_use = m_new == -INFINITY ? 0.f : m_new;
-            const float alpha = fast_exp2(m_i - m_use);
-            m_i = m_new;
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                mx = fmaxf(mx, s[kb][r]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mc = mx * scale_log2;  // log2-domain tile maximum
 
-            float psum = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float p = fast_exp2(s[kb][r] - m_use);
-                    s[kb][r] = p;
-                    psum += p;
-                }
-            l_i = l_i * alpha + psum;
+        // Lazy rescale: only when some lane's maximum grew past the slack.
+        if (__any(mc > m_i + kRescaleSlack)) {
+            const float m_new = fmaxf(m_i, mc);
+            const float alpha = fast_exp2(m_i - (m_new == -INFINITY ? 0.f : m_new));
+            l_i *= alpha;
 #pragma unroll
             for (int db = 0; db < DB; ++db)
                 acc[db] *= alpha;
-
-            // O^T += V^T P^T.  B operand (kb, t2): registers 8*t2..8*t2+7 of
-            // s[kb], i.e. keys kb*32 + 16*t2 + 4g + {0..3} and the same + 8.
-            bf16x8 pb[2][2];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int t2 = 0; t2 < 2; ++t2)
-                    pb[kb][t2] = pack8(s[kb], 8 * t2);
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int t2 = 0; t2 < 2; ++t2) {
-                        const uint16_t *row = vt + (db * 32 + l32) * T::VP + kb * 32 + 16 * t2 + 4 * g;
-                        const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(row);
-                        const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(row + 8);
-                        acc[db] = mfma32(join(lo, hi), pb[kb][t2], acc[db]);
-                    }
+            m_i = m_new;
         }
+        const float neg_m = m_i == -INFINITY ? 0.f : -m_i;
 
+        float psum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float p = fast_exp2(fmaf(s[kb][r], scale_log2, neg_m));
+                s[kb][r] = p;
+                psum += p;
+            }
+        l_i += psum;
+
+        // O^T += V^T P^T.  B operand (kb, t2): registers 8*t2..8*t2+7 of
+        // s[kb] = keys kb*32 + 16*t2 + 4g + {0..3} and the same + 8; the A
+        // operand reads exactly those keys transposed from the V tile.
+        bf16x8 pb[2][2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2)
+                pb[kb][t2] = pack8(s[kb], 8 * t2);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const uint16_t *vr = vt + (kb * 32 + 16 * t2) * D;
+                    const bf16x8 a = join(lds_tr4(vr + voff[db][0]), lds_tr4(vr + voff[db][1]));
+                    acc[db] = mfma32(a, pb[kb][t2], acc[db]);
+                }
+    };
+
+    issue(t_begin, lds);
+    wait_vmem();
+    __syncthreads();
+    for (int t = t_begin;;) {
         if (t < t_end)
-            commit(buf ^ 1);
+            issue(t + 1, lds + T::STAGE);
+        compute(t, IC<0>{});
+        wait_vmem();
         __syncthreads();
-        buf ^= 1;
+        if (t == t_end)
+            break;
+        ++t;
+        if (t < t_end)
+            issue(t + 1, lds);
+        compute(t, IC<1>{});
+        wait_vmem();
+        __syncthreads();
+        if (t == t_end)
+            break;
+        ++t;
     }
 
     if (!q_ok)
@@ -236,6 +254,18 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     if (g == 0)
         LSE[(static_cast<long long>(b) * L + my_q) * H + h] = (m_i + log2f(l_tot)) * kLn2;
 }
+
+// Explicit instantiations: the host-side launch stubs are emitted here
+// unconditionally (clang's host pass does not always emit them for templates
+// only referenced through a function pointer).
+template __global__ void fwd_kernel<64>(const uint16_t *__restrict__, const uint16_t *__restrict__,
+                                        const uint16_t *__restrict__, uint16_t *__restrict__,
+                                        float *__restrict__, int, int, int, int,
+                                        const int32_t *__restrict__, int, float, int);
+template __global__ void fwd_kernel<128>(const uint16_t *__restrict__, const uint16_t *__restrict__,
+                                         const uint16_t *__restrict__, uint16_t *__restrict__,
+                                         float *__restrict__, int, int, int, int,
+                                         const int32_t *__restrict__, int, float, int);
 
 template <int D>
 static int launch_fwd_d(const FwdArgs &a)
