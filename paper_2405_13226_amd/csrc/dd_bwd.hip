@@ -181,16 +181,14 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             dma_row_f32(fs + T::BM, dlt, i0, L, lane);
     };
 
-    auto compute = [&](int t, auto bufc) {
+    // One tile; MASKED selects the boundary-tile variant at compile time.
+    auto body = [&](int i0, auto bufc, auto maskc) {
         constexpr int BUF = decltype(bufc)::value;
+        constexpr bool MASKED = decltype(maskc)::value != 0;
         const uint16_t *qs = lds + BUF * T::STAGE;
         const uint16_t *dos = qs + T::TILE;
         const float *lse_s = reinterpret_cast<const float *>(qs + 2 * T::TILE);
         const float *dlt_s = lse_s + T::BM;
-        const int i0 = t * T::BM;
-        if (!(wave_on && i0 <= hi_w && i0 + T::BM - 1 >= lo_w))
-            return;
-        const bool full = wave_full_keys && i0 >= lo_all && i0 + T::BM - 1 <= hi_all;
 
         // S = Q K^T and dP = dO V^T for two 32-query blocks
         // (C layout: column = this lane's key, rows = queries).
@@ -220,7 +218,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                 for (int e = 0; e < 4; ++e) {
                     const int r = 4 * rg + e;
                     float p = fast_exp2(fmaf(s[qb][r], scale_log2, -lz[e]));
-                    if (!full) {
+                    if constexpr (MASKED) {
                         const int qr = qb * 32 + 8 * rg + e;
                         const bool ok = (qr >= qlo_r) & (qr <= qhi_r);
                         p = ok ? p : 0.f;
@@ -255,6 +253,16 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     dv[db] = mfma32(ado, pb[qb][t2], dv[db]);
                     dk[db] = mfma32(aq, sb[qb][t2], dk[db]);
                 }
+    };
+
+    auto compute = [&](int t, auto bufc) {
+        const int i0 = t * T::BM;
+        if (!(wave_on && i0 <= hi_w && i0 + T::BM - 1 >= lo_w))
+            return;
+        if (wave_full_keys && i0 >= lo_all && i0 + T::BM - 1 <= hi_all)
+            body(i0, bufc, IC<0>{});
+        else
+            body(i0, bufc, IC<1>{});
     };
 
     issue(t_begin, lds);
@@ -392,14 +400,12 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         plan.issue(stage + T::TILE, Vb, rs, t * T::BN, L, wave, lane);
     };
 
-    auto compute = [&](int t, auto bufc) {
+    // One tile; MASKED selects the boundary-tile variant at compile time.
+    auto body = [&](int j0, auto bufc, auto maskc) {
         constexpr int BUF = decltype(bufc)::value;
+        constexpr bool MASKED = decltype(maskc)::value != 0;
         const uint16_t *ks = lds + BUF * T::STAGE;
         const uint16_t *vs = ks + T::TILE;
-        const int j0 = t * T::BN;
-        if (!(wave_on && j0 <= hi_w && j0 + T::BN - 1 >= lo_w))
-            return;
-        const bool full = wave_full_rows && j0 >= lo_all && j0 + T::BN - 1 <= hi_all;
 
         // S^T = K Q^T and dP^T = V dO^T (column = this lane's query).
         f32x16 s[2], dp[2];
@@ -420,7 +426,7 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 float p = fast_exp2(fmaf(s[kb][r], scale_log2, neg_lse2));
-                if (!full) {
+                if constexpr (MASKED) {
                     const int kr = kb * 32 + 8 * (r >> 2) + (r & 3);
                     const bool ok = (kr >= lo_r) & (kr <= hi_r);
                     p = ok ? p : 0.f;
@@ -445,6 +451,16 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     const bf16x8 a = join(lds_tr4(kr + toff[db][0]), lds_tr4(kr + toff[db][1]));
                     dq[db] = mfma32(a, sb[kb][t2], dq[db]);
                 }
+    };
+
+    auto compute = [&](int t, auto bufc) {
+        const int j0 = t * T::BN;
+        if (!(wave_on && j0 <= hi_w && j0 + T::BN - 1 >= lo_w))
+            return;
+        if (wave_full_rows && j0 >= lo_all && j0 + T::BN - 1 <= hi_all)
+            body(j0, bufc, IC<0>{});
+        else
+            body(j0, bufc, IC<1>{});
     };
 
     issue(t_begin, lds);

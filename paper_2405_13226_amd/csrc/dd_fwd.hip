@@ -131,14 +131,12 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         plan.issue(stage + T::TILE, Vb, rs, t * T::BN, L, wave, lane);
     };
 
-    auto compute = [&](int t, auto bufc) {
+    // One tile; MASKED selects the boundary-tile variant at compile time.
+    auto body = [&](int j0, auto bufc, auto maskc) {
         constexpr int BUF = decltype(bufc)::value;
+        constexpr bool MASKED = decltype(maskc)::value != 0;
         const uint16_t *kt = lds + BUF * T::STAGE;
         const uint16_t *vt = kt + T::TILE;
-        const int j0 = t * T::BN;
-        if (!(wave_on && j0 <= hi_w && j0 + T::BN - 1 >= lo_w))
-            return;
-        const bool full = wave_full_rows && j0 >= lo_all && j0 + T::BN - 1 <= hi_all;
 
         // S^T = K Q^T for two 32-key blocks.
         f32x16 s[2];
@@ -151,7 +149,7 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         }
 
         // Boundary tiles: keys outside [lo_q, hi_q] -> -inf (branch-free).
-        if (!full) {
+        if constexpr (MASKED) {
             const int lo_r = lo_q - j0 - 4 * g, hi_r = hi_q - j0 - 4 * g;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -213,6 +211,16 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     const bf16x8 a = join(lds_tr4(vr + voff[db][0]), lds_tr4(vr + voff[db][1]));
                     acc[db] = mfma32(a, pb[kb][t2], acc[db]);
                 }
+    };
+
+    auto compute = [&](int t, auto bufc) {
+        const int j0 = t * T::BN;
+        if (!(wave_on && j0 <= hi_w && j0 + T::BN - 1 >= lo_w))
+            return;
+        if (wave_full_rows && j0 >= lo_all && j0 + T::BN - 1 <= hi_all)
+            body(j0, bufc, IC<0>{});
+        else
+            body(j0, bufc, IC<1>{});
     };
 
     issue(t_begin, lds);
