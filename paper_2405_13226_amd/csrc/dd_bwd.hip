@@ -4,9 +4,10 @@
 // Three launches on the caller's stream:
 //   1. prep:  delta_i = sum_d dO_id O_id and LSE in log2 units, both fp32 in
 //             a [B*H][L] workspace (one contiguous row per (b, h)).
-//   2. dkdv:  key-resident.  One workgroup = 4 waves = 128 keys; each wave
-//             keeps its 32 keys' K and V rows in registers.  It walks the
-//             query tiles (64 queries) its keys are visible to and forms
+//   2. dkdv:  key-resident.  One workgroup = 8 waves = 128 keys; the two
+//             waves of a 32-key group keep K (one) and V (the other) rows in
+//             registers.  They walk the query tiles (64 queries) their keys
+//             are visible to and form
 //               S = Q K^T, P = exp2(S*scale*log2e - lse2), dP = dO V^T,
 //               dS = P * (dP - delta),
 //               dV^T += dO^T P,  dK^T += Q^T dS.
@@ -77,13 +78,26 @@ template <int D>
 struct KvTile {
     static constexpr int BN = 128;            // keys per workgroup
     static constexpr int BM = 64;             // queries per tile
+    static constexpr int NW = 8;              // waves: 4 key groups x 2 roles
     static constexpr int TILE = BM * D;       // elements of a Q or dO tile
     // Q tile, dO tile, then lse2[BM] and delta[BM] as floats.
     static constexpr int STAGE = 2 * TILE + 2 * BM * 2;
+    // P hand-off between the two waves of a key group: per group, 32 fp32
+    // per lane (two 32-query blocks x 16 C-layout registers), 8 KiB.
+    static constexpr int PBUF_FLOATS = 4 * 64 * 32;
 };
 
+// Key-resident dK/dV.  The 32 keys of a group are shared by two waves on the
+// same SIMD (wave w and w + 4):
+//   role A (waves 0-3): K in registers; S = Q K^T, P = exp2(S*c - lse2)
+//                       (masked), P handed to role B through LDS,
+//                       dV^T += dO^T P;
+//   role B (waves 4-7): V in registers; dP = dO V^T, then dS = P (dP - delta),
+//                       dK^T += Q^T dS.
+// Each wave holds one accumulator set, so two waves fit per SIMD and one
+// wave's softmax arithmetic overlaps the other's matrix products.
 template <int D>
-__global__ void __launch_bounds__(256, 1)
+__global__ void __launch_bounds__(512, 1)
 dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
             const float *__restrict__ lse2g, const float *__restrict__ deltag,
@@ -95,13 +109,272 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     constexpr int KK = D / 16;
     constexpr int DB = D / 32;
     __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE];
+    __shared__ __attribute__((aligned(16))) float pbuf[T::PBUF_FLOATS];
+
+    const bool causal = causal_i != 0;
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
+    const int grp = wave & 3;
+    const bool role_a = wave < 4;
+
+    // Key blocks in ascending order: under the causal mask the first blocks
+    // of a row see the most queries, so the heaviest work starts first.
+    const int BH = B * H;
+    const int kvb = blockIdx.x / BH;
+    const int bh = blockIdx.x % BH;
+    const int b = bh / H, h = bh % H;
+
+    const long long rs = static_cast<long long>(H) * D;
+    const long long base = (static_cast<long long>(b) * L * H + h) * D;
+    const uint16_t *Qb = Q + base, *dOb = dO + base;
+    const float *lse2 = lse2g + static_cast<long long>(bh) * L;
+    const float *dlt = deltag + static_cast<long long>(bh) * L;
+
+    const int k0w = kvb * T::BN + grp * 32;
+    const int my_k = k0w + l32;
+    const bool k_ok = my_k < L;
+    int qlo_k = 1, qhi_k = 0;
+    if (k_ok)
+        key_queries(b, L, my_k, causal, cu, n_docs, qlo_k, qhi_k);
+    const bool wave_on = k0w < L;
+    const int lo_w = wave_min(k_ok ? qlo_k : 0x7fffffff);
+    const int hi_w = wave_max(k_ok ? qhi_k : -1);
+    const int lo_all = wave_max(k_ok ? qlo_k : -1);
+    const int hi_all = wave_min(k_ok ? qhi_k : 0x7fffffff);
+    const bool wave_full_keys = (k0w + 31) < L;
+
+    const int kf0 = kvb * T::BN, kl = min(kvb * T::BN + T::BN - 1, L - 1);
+    int wlo, whi, tmp;
+    key_queries(b, L, kf0, causal, cu, n_docs, wlo, tmp);
+    key_queries(b, L, kl, causal, cu, n_docs, tmp, whi);
+    const int t_begin = wlo / T::BM, t_end = whi / T::BM;
+
+    // Role A keeps K rows, role B keeps V rows of this lane's key
+    // (B operands: column = key).
+    bf16x8 kv[KK];
+    {
+        const uint16_t *src = (role_a ? K : V) + base + my_k * rs + g * 8;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            u32x4 v = u32x4{0u, 0u, 0u, 0u};
+            if (k_ok)
+                v = *reinterpret_cast<const u32x4 *>(src + kk * 16);
+            kv[kk] = as_bf16x8(v);
+        }
+    }
+
+    // Per-lane LDS offsets: row reads (row l32 of a 32-query block, chunk
+    // 2*kk + g) and transposed reads (rows 8*hh + 4*g + e of a 16-query step,
+    // columns db*32 + 16*(G&1) + 4*c), shared by the Q and dO tiles.
+    int roff[KK], toff[DB][2];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+        roff[kk] = tile_off<D>(l32, kk * 16 + g * 8);
+    {
+        const int G = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G & 1) + 4 * c);
+    }
+    // This lane's slot of the P hand-off buffer: [grp][reg/4][lane][4].
+    float *pslot = pbuf + grp * 64 * 32 + lane * 4;
+
+    f32x16 acc[DB];  // dV^T (role A) or dK^T (role B)
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+        acc[db] = f32x16{};
+
+    DmaPlan<D, T::BM, T::NW> plan;
+    plan.init(rs, wave, lane);
+    auto issue = [&](int t, uint16_t *stage) {
+        const int i0 = t * T::BM;
+        plan.issue(stage, Qb, rs, i0, L, wave, lane);
+        plan.issue(stage + T::TILE, dOb, rs, i0, L, wave, lane);
+        float *fs = reinterpret_cast<float *>(stage + 2 * T::TILE);
+        if (wave == 0)
+            dma_row_f32(fs, lse2, i0, L, lane);
+        else if (wave == 1)
+            dma_row_f32(fs + T::BM, dlt, i0, L, lane);
+    };
+
+    // Transposed A operand (rows of the 16-query step of (qb, t2)) times a
+    // bf16 B operand, accumulated into acc.
+    auto tr_products = [&](const uint16_t *tile, const bf16x8 (&bop)[2][2]) {
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const uint16_t *tr = tile + (qb * 32 + 16 * t2) * D;
+                    const bf16x8 a = join(lds_tr4(tr + toff[db][0]), lds_tr4(tr + toff[db][1]));
+                    acc[db] = mfma32(a, bop[qb][t2], acc[db]);
+                }
+    };
+
+    // Row-wise products X K^T (role A, X = Q) or X V^T (role B, X = dO).
+    auto row_products = [&](const uint16_t *tile, f32x16 (&c)[2]) {
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            c[qb] = f32x16{};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk)
+                c[qb] = mfma32(lds_row8(tile + qb * 32 * D + roff[kk]), kv[kk], c[qb]);
+        }
+    };
+
+    // Phase 1 of a tile.  Role A: S, P (masked when MASKED), P to LDS and
+    // to bf16.  Role B: dP.  Phase 2 (after a barrier): role A dV, role B
+    // dS and dK.
+    auto body = [&](int i0, auto bufc, auto maskc, bool active) {
+        constexpr int BUF = decltype(bufc)::value;
+        constexpr bool MASKED = decltype(maskc)::value != 0;
+        const uint16_t *qs = lds + BUF * T::STAGE;
+        const uint16_t *dos = qs + T::TILE;
+        const float *lse_s = reinterpret_cast<const float *>(qs + 2 * T::TILE);
+        const float *dlt_s = lse_s + T::BM;
+        f32x16 c[2];
+        bf16x8 bop[2][2];
+        if (role_a) {
+            if (active) {
+                row_products(qs, c);
+                const int qlo_r = qlo_k - i0 - 4 * g, qhi_r = qhi_k - i0 - 4 * g;
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+                    for (int rg = 0; rg < 4; ++rg) {
+                        const f32x4 lz = *reinterpret_cast<const f32x4 *>(
+                            lse_s + qb * 32 + 8 * rg + 4 * g);
+                        f32x4 pv;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            float p = fast_exp2(fmaf(c[qb][4 * rg + e], scale_log2, -lz[e]));
+                            if constexpr (MASKED) {
+                                const int qr = qb * 32 + 8 * rg + e;
+                                const bool ok = (qr >= qlo_r) & (qr <= qhi_r);
+                                p = ok ? p : 0.f;
+                            }
+                            c[qb][4 * rg + e] = p;
+                            pv[e] = p;
+                        }
+                        *reinterpret_cast<f32x4 *>(pslot + (qb * 4 + rg) * 256) = pv;
+                    }
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+                    for (int t2 = 0; t2 < 2; ++t2)
+                        bop[qb][t2] = pack8(c[qb], 8 * t2);
+            }
+            __syncthreads();  // P visible to role B
+            if (active)
+                tr_products(dos, bop);  // dV^T += dO^T P
+        } else {
+            if (active)
+                row_products(dos, c);  // dP
+            __syncthreads();
+            if (active) {
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+                    for (int rg = 0; rg < 4; ++rg) {
+                        const f32x4 dz = *reinterpret_cast<const f32x4 *>(
+                            dlt_s + qb * 32 + 8 * rg + 4 * g);
+                        const f32x4 pv = *reinterpret_cast<const f32x4 *>(pslot + (qb * 4 + rg) * 256);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            c[qb][4 * rg + e] = pv[e] * (c[qb][4 * rg + e] - dz[e]);
+                    }
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+                    for (int t2 = 0; t2 < 2; ++t2)
+                        bop[qb][t2] = pack8(c[qb], 8 * t2);
+                tr_products(qs, bop);  // dK^T += Q^T dS
+            }
+        }
+    };
+
+    // The pair of waves of a key group shares one activity decision; every
+    // wave reaches the mid-tile barrier.
+    auto compute = [&](int t, auto bufc) {
+        const int i0 = t * T::BM;
+        const bool active = wave_on && i0 <= hi_w && i0 + T::BM - 1 >= lo_w;
+        if (wave_full_keys && i0 >= lo_all && i0 + T::BM - 1 <= hi_all)
+            body(i0, bufc, IC<0>{}, active);
+        else
+            body(i0, bufc, IC<1>{}, active);
+    };
+
+    issue(t_begin, lds);
+    wait_vmem();
+    __syncthreads();
+    for (int t = t_begin;;) {
+        if (t < t_end)
+            issue(t + 1, lds + T::STAGE);
+        compute(t, IC<0>{});
+        wait_vmem();
+        __syncthreads();
+        if (t == t_end)
+            break;
+        ++t;
+        if (t < t_end)
+            issue(t + 1, lds);
+        compute(t, IC<1>{});
+        wait_vmem();
+        __syncthreads();
+        if (t == t_end)
+            break;
+        ++t;
+    }
+
+    if (!k_ok)
+        return;
+    const float osc = role_a ? 1.0f : scale;
+    uint16_t *dst = (role_a ? dV : dK) + base + my_k * rs;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+            const int d = db * 32 + 8 * rg + 4 * g;
+            *reinterpret_cast<bf16x4 *>(dst + d) =
+                pack4(acc[db][4 * rg] * osc, acc[db][4 * rg + 1] * osc,
+                      acc[db][4 * rg + 2] * osc, acc[db][4 * rg + 3] * osc);
+        }
+}
+
+// Key-resident dK/dV for small head dims: one wave owns the 32 keys of a
+// group with both K and V in registers and both accumulators, and walks the
+// 64-query tile as two 32-query halves to keep its live registers low enough
+// for several waves per SIMD.
+template <int D>
+struct KvTile1 {
+    static constexpr int BN = 128;            // keys per workgroup
+    static constexpr int BM = 64;             // queries per tile
+    static constexpr int NW = 4;
+    static constexpr int TILE = BM * D;
+    static constexpr int STAGE = 2 * TILE + 2 * BM * 2;
+};
+
+template <int D>
+__global__ void __launch_bounds__(256, 2)
+dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
+             const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
+             const float *__restrict__ lse2g, const float *__restrict__ deltag,
+             uint16_t *__restrict__ dK, uint16_t *__restrict__ dV, int B, int L, int H,
+             int causal_i, const int32_t *__restrict__ cu, int n_docs, float scale_log2,
+             float scale, int nkb)
+{
+    using T = KvTile1<D>;
+    constexpr int KK = D / 16;
+    constexpr int DB = D / 32;
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE];
 
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
 
-    // Key blocks in ascending order: under the causal mask the first blocks
-    // of a row see the most queries, so the heaviest work starts first.
     const int BH = B * H;
     const int kvb = blockIdx.x / BH;
     const int bh = blockIdx.x % BH;
@@ -132,7 +405,6 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     key_queries(b, L, kl, causal, cu, n_docs, tmp, whi);
     const int t_begin = wlo / T::BM, t_end = whi / T::BM;
 
-    // K and V rows of this lane's key (B operands: column = key).
     bf16x8 kf[KK], vf[KK];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
@@ -145,9 +417,6 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         vf[kk] = as_bf16x8(vv);
     }
 
-    // Per-lane LDS offsets: row reads (row l32 of a 32-query block, chunk
-    // 2*kk + g) and transposed reads (rows 8*hh + 4*g + e of a 16-query step,
-    // columns db*32 + 16*(G&1) + 4*c), shared by the Q and dO tiles.
     int roff[KK], toff[DB][2];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk)
@@ -168,7 +437,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         dv[db] = f32x16{};
     }
 
-    DmaPlan<D, T::BM, 4> plan;
+    DmaPlan<D, T::BM, T::NW> plan;
     plan.init(rs, wave, lane);
     auto issue = [&](int t, uint16_t *stage) {
         const int i0 = t * T::BM;
@@ -181,7 +450,6 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             dma_row_f32(fs + T::BM, dlt, i0, L, lane);
     };
 
-    // One tile; MASKED selects the boundary-tile variant at compile time.
     auto body = [&](int i0, auto bufc, auto maskc) {
         constexpr int BUF = decltype(bufc)::value;
         constexpr bool MASKED = decltype(maskc)::value != 0;
@@ -189,26 +457,16 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const uint16_t *dos = qs + T::TILE;
         const float *lse_s = reinterpret_cast<const float *>(qs + 2 * T::TILE);
         const float *dlt_s = lse_s + T::BM;
-
-        // S = Q K^T and dP = dO V^T for two 32-query blocks
-        // (C layout: column = this lane's key, rows = queries).
-        f32x16 s[2], dp[2];
+        const int qlo_r = qlo_k - i0 - 4 * g, qhi_r = qhi_k - i0 - 4 * g;
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-            s[qb] = f32x16{};
-            dp[qb] = f32x16{};
+            f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
                 const int off = qb * 32 * D + roff[kk];
-                s[qb] = mfma32(lds_row8(qs + off), kf[kk], s[qb]);
-                dp[qb] = mfma32(lds_row8(dos + off), vf[kk], dp[qb]);
+                s = mfma32(lds_row8(qs + off), kf[kk], s);
+                dp = mfma32(lds_row8(dos + off), vf[kk], dp);
             }
-        }
-
-        // P = exp2(S*c - lse2) and dS = P (dP - delta), in place.
-        const int qlo_r = qlo_k - i0 - 4 * g, qhi_r = qhi_k - i0 - 4 * g;
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
             for (int rg = 0; rg < 4; ++rg) {
                 const int ql = qb * 32 + 8 * rg + 4 * g;
@@ -217,32 +475,19 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int r = 4 * rg + e;
-                    float p = fast_exp2(fmaf(s[qb][r], scale_log2, -lz[e]));
+                    float p = fast_exp2(fmaf(s[r], scale_log2, -lz[e]));
                     if constexpr (MASKED) {
                         const int qr = qb * 32 + 8 * rg + e;
                         const bool ok = (qr >= qlo_r) & (qr <= qhi_r);
                         p = ok ? p : 0.f;
                     }
-                    s[qb][r] = p;
-                    dp[qb][r] = p * (dp[qb][r] - dz[e]);
+                    s[r] = p;
+                    dp[r] = p * (dp[r] - dz[e]);
                 }
             }
-
-        // dV^T += dO^T P and dK^T += Q^T dS.  B operand (qb, t2): rows
-        // 8*t2..8*t2+7 of the C layout = queries qb*32+16*t2+4g+{0..3}, +8;
-        // the A operands read exactly those queries transposed.
-        bf16x8 pb[2][2], sb[2][2];
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
             for (int t2 = 0; t2 < 2; ++t2) {
-                pb[qb][t2] = pack8(s[qb], 8 * t2);
-                sb[qb][t2] = pack8(dp[qb], 8 * t2);
-            }
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-            for (int t2 = 0; t2 < 2; ++t2)
+                const bf16x8 pb = pack8(s, 8 * t2), sb = pack8(dp, 8 * t2);
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
                     const int ro = (qb * 32 + 16 * t2) * D;
@@ -250,9 +495,11 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                                             lds_tr4(dos + ro + toff[db][1]));
                     const bf16x8 aq = join(lds_tr4(qs + ro + toff[db][0]),
                                            lds_tr4(qs + ro + toff[db][1]));
-                    dv[db] = mfma32(ado, pb[qb][t2], dv[db]);
-                    dk[db] = mfma32(aq, sb[qb][t2], dk[db]);
+                    dv[db] = mfma32(ado, pb, dv[db]);
+                    dk[db] = mfma32(aq, sb, dk[db]);
                 }
+            }
+        }
     };
 
     auto compute = [&](int t, auto bufc) {
@@ -502,24 +749,28 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 // Explicit instantiations: the host-side launch stubs of these kernel
 // templates are emitted here unconditionally (clang's host pass does not
 // always emit them for templates only referenced through a function pointer).
-#define DD_BWD_INSTANTIATE(D)                                                                    \
-    template __global__ void prep_kernel<D>(const uint16_t *__restrict__,                       \
-                                            const uint16_t *__restrict__,                       \
-                                            const float *__restrict__, float *__restrict__,     \
-                                            float *__restrict__, int, int, int);                \
-    template __global__ void dkdv_kernel<D>(                                                     \
-        const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__, \
+#define DD_KV_ARGS                                                                               \
+    const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,   \
         const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,      \
         uint16_t *__restrict__, uint16_t *__restrict__, int, int, int, int,                      \
-        const int32_t *__restrict__, int, float, float, int);                                    \
-    template __global__ void dq_kernel<D>(                                                       \
-        const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__, \
+        const int32_t *__restrict__, int, float, float, int
+#define DD_Q_ARGS                                                                                \
+    const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,   \
         const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,      \
         uint16_t *__restrict__, int, int, int, int, const int32_t *__restrict__, int, float,     \
-        float, int);
-DD_BWD_INSTANTIATE(64)
-DD_BWD_INSTANTIATE(128)
-#undef DD_BWD_INSTANTIATE
+        float, int
+#define DD_PREP_ARGS                                                                             \
+    const uint16_t *__restrict__, const uint16_t *__restrict__, const float *__restrict__,      \
+        float *__restrict__, float *__restrict__, int, int, int
+template __global__ void prep_kernel<64>(DD_PREP_ARGS);
+template __global__ void prep_kernel<128>(DD_PREP_ARGS);
+template __global__ void dkdv1_kernel<64>(DD_KV_ARGS);   // D = 64: single-role waves
+template __global__ void dkdv_kernel<128>(DD_KV_ARGS);   // D = 128: paired waves
+template __global__ void dq_kernel<64>(DD_Q_ARGS);
+template __global__ void dq_kernel<128>(DD_Q_ARGS);
+#undef DD_KV_ARGS
+#undef DD_Q_ARGS
+#undef DD_PREP_ARGS
 
 // ---------------------------------------------------------------------------
 template <int D>
@@ -546,9 +797,16 @@ static int launch_bwd_d(const BwdArgs &a)
     const int nkb = (a.L + KvTile<D>::BN - 1) / KvTile<D>::BN;
     {
         ProfScope prof(K_DKDV, st);
-        e = launch_kernel(dkdv_kernel<D>, dim3(static_cast<unsigned>(nkb * a.B * a.H)), dim3(256),
-                          st, a.Q, a.K, a.V, a.dO, lse2, delta, a.dK, a.dV, a.B, a.L, a.H,
-                          a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, scale, nkb);
+        if constexpr (D == 64)
+            e = launch_kernel(dkdv1_kernel<D>, dim3(static_cast<unsigned>(nkb * a.B * a.H)),
+                              dim3(64 * KvTile1<D>::NW), st, a.Q, a.K, a.V, a.dO, lse2, delta,
+                              a.dK, a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs,
+                              scale_log2, scale, nkb);
+        else
+            e = launch_kernel(dkdv_kernel<D>, dim3(static_cast<unsigned>(nkb * a.B * a.H)),
+                              dim3(64 * KvTile<D>::NW), st, a.Q, a.K, a.V, a.dO, lse2, delta,
+                              a.dK, a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs,
+                              scale_log2, scale, nkb);
     }
     if (e != hipSuccess)
         return DD_ERR_HIP;
