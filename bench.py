@@ -9,7 +9,9 @@ Workloads (``--workload``):
   dd_sweep_d64   (default) buckets L = 256 .. 8192, B = 65536 / L, H = 16, D = 64
   dd_sweep_d128  the same with D = 128
   chunk_vs_dd    8 x 8192 chunks of log-normal documents: dense causal,
-                 document-masked, and the DD buckets of the same documents
+                 document-masked, the DD buckets of the same documents (one
+                 launch per bucket), and the same DD pieces packed into one
+                 document-masked launch
   stream         64 steps with L drawn from 256 .. 16384, weights 1/L, D = 128
   tiny           B = 4, L = 256, H = 4, D = 64
 
@@ -89,10 +91,15 @@ def workload(name, seed, buckets=None):
                   dict(name="masked 8x8192", B=8, L=8192, cu=cu, variant="masked")]
         for n, b in dd.decompose(docs, min_len=256, max_len=8192).items():
             groups.append(dict(name=f"DD L={n}", B=b.count, L=n, cu=None, variant="dd"))
+        packed = dd.pack_step(docs, min_len=256, max_len=8192)
+        groups.append(dict(name="DD packed 1x", B=1, L=packed.tokens, cu=packed.cu_doclens,
+                           variant="dd_packed"))
         desc = dict(workload=name, tokens_per_group=TOKENS, H=H, D=D, causal=True,
                     documents=int(len(docs)), doc_seed=seed,
                     dd_tokens_kept=int(sum(g["B"] * g["L"] for g in groups
-                                           if g.get("variant") == "dd")))
+                                           if g.get("variant") == "dd")),
+                    note="one bench step runs every variant once; compare the variants' "
+                         "ms (dense, masked, the sum of the dd buckets, dd_packed)")
     else:  # stream
         H, D = 16, 128
         lens = synth.length_stream(seed, steps=64)

@@ -11,6 +11,9 @@
 * ``chunk_doclens``: the concat-and-chunk baseline (Sec. 1) -- documents are
   concatenated and cut into fixed-length rows; the document boundaries become
   the ``cu_doclens`` offsets of the document-masked attention.
+* ``pack_step``: every DD piece of a step packed into one row with piece
+  boundaries as ``cu_doclens``, so the whole DD step runs as a single
+  document-masked launch instead of one launch per bucket.
 * ``useful_pairs`` / ``attention_flops``: the work the masked attention must
   do.  A token at context position j (Appendix F) attends to j + 1 keys, so a
   causal segment of length l has l(l+1)/2 (query, key) pairs per head.
@@ -113,3 +116,41 @@ def attention_bytes(B: int, L: int, H: int, D: int) -> tuple:
     t = B * L * H * D * 2
     s = B * L * H * 4
     return 4 * t + s, 8 * t + s
+
+
+@dataclass
+class PackedStep:
+    """All DD pieces of a step packed into one row, ready for one masked launch.
+
+    ``src`` gives, for every packed token, its position in the concatenated
+    document stream; ``cu_doclens`` marks the piece boundaries of the packed
+    row.  Attention of the packed row under the document mask is exactly the
+    per-bucket DD attention: pieces never attend to each other.  Pieces are
+    ordered shortest first, so the heaviest query blocks (the ends of the
+    longest pieces) come last, where the kernels' heaviest-first block order
+    starts.  With every piece length a multiple of 128, no 128-query or 64-key
+    tile of the kernels straddles two pieces.
+    """
+
+    src: np.ndarray
+    cu_doclens: np.ndarray
+    lengths: np.ndarray
+
+    @property
+    def tokens(self) -> int:
+        return int(self.src.size)
+
+
+def pack_step(doc_lengths, min_len: int = 256, max_len: int | None = 8192) -> PackedStep:
+    """Pack the binary-decomposition pieces of ``doc_lengths`` into one row."""
+    buckets = decompose(doc_lengths, min_len, max_len)
+    starts, lens = [], []
+    for n in sorted(buckets):
+        for s in buckets[n].starts:
+            starts.append(int(s))
+            lens.append(int(n))
+    lens_a = np.asarray(lens, dtype=np.int64)
+    src = np.concatenate([np.arange(s, s + n, dtype=np.int64) for s, n in zip(starts, lens)]) \
+        if lens else np.zeros(0, dtype=np.int64)
+    cu = np.concatenate([[0], np.cumsum(lens_a)]).astype(np.int32)
+    return PackedStep(src=src, cu_doclens=cu, lengths=lens_a)

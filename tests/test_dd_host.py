@@ -68,3 +68,24 @@ def test_flops_and_bytes():
     fb, bb = dd.attention_bytes(256, 256, 16, 64)
     t = 65536 * 16 * 64 * 2
     assert fb == 4 * t + 65536 * 16 * 4 and bb == 8 * t + 65536 * 16 * 4
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_packed_step_matches_buckets(seed):
+    lens = synth.lognormal_doc_lengths(seed)
+    packed = dd.pack_step(lens, min_len=256, max_len=8192)
+    buckets = dd.decompose(lens, min_len=256, max_len=8192)
+    assert packed.tokens == sum(n * b.count for n, b in buckets.items())
+    # every packed piece is a contiguous run of source tokens of its bucket length
+    cu = packed.cu_doclens
+    assert cu[0] == 0 and cu[-1] == packed.tokens and np.all(np.diff(cu) >= 256)
+    assert np.all(cu % 128 == 0)  # no kernel tile straddles two pieces
+    for a, z in zip(cu[:-1], cu[1:]):
+        run = packed.src[a:z]
+        assert np.all(np.diff(run) == 1)
+    # shortest pieces first
+    assert np.all(np.diff(packed.lengths) >= 0)
+    # the same multiset of pieces as the per-bucket decomposition
+    got = sorted(zip(packed.src[cu[:-1]].tolist(), np.diff(cu).tolist()))
+    ref = sorted((int(s), n) for n, b in buckets.items() for s in b.starts)
+    assert got == ref

@@ -157,3 +157,28 @@ def test_errors_with_live_device(cuda):
                               x["q"].data_ptr(), lse.data_ptr(), 1, 64, 1, 64, 1, None, 0, None)
     assert st == 7  # O aliases Q
     del o
+
+
+def test_packed_dd_step_equals_bucket_launches(cuda):
+    # N1: all DD pieces of a step in one document-masked launch give the same
+    # results as one launch per bucket.
+    H, D = 2, 64
+    lens = synth.lognormal_doc_lengths(3, total_tokens=8192, median=500)
+    packed = dd.dd.pack_step(lens, min_len=128, max_len=2048)
+    x = inputs(1, 8192, H, D, 10, cuda)
+    flat = {n: t.view(8192, H, D) for n, t in x.items()}
+    src = torch.from_numpy(packed.src).to(cuda)
+    pk = {n: t.index_select(0, src).unsqueeze(0).contiguous() for n, t in flat.items()}
+    o, lse = dd.forward(pk["q"], pk["k"], pk["v"], cu_doclens=packed.cu_doclens)
+    g = dd.backward(pk["q"], pk["k"], pk["v"], o, lse, pk["do"], cu_doclens=packed.cu_doclens)
+    cu = packed.cu_doclens
+    for n in sorted(set(packed.lengths.tolist())):
+        idx = [i for i in range(len(cu) - 1) if cu[i + 1] - cu[i] == n]
+        rows = torch.cat([torch.arange(int(cu[i]), int(cu[i + 1])) for i in idx]).to(cuda)
+        bk = {k: t[0].index_select(0, rows).view(len(idx), n, H, D).contiguous() for k, t in pk.items()}
+        ob, lb = dd.forward(bk["q"], bk["k"], bk["v"])
+        gb = dd.backward(bk["q"], bk["k"], bk["v"], ob, lb, bk["do"])
+        assert (o[0].index_select(0, rows).view(len(idx), n, H, D).float() - ob.float()).abs().max().item() <= 1e-2
+        for a, b in zip(g, gb):
+            assert rel_l2(a[0].index_select(0, rows).float().cpu().numpy().ravel(),
+                          b.float().cpu().numpy().ravel()) <= 1e-2
