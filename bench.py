@@ -44,6 +44,37 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def kernel_source_hash():
+    """sha256 of the HIP sources: counter-based traffic is void once they change."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2405_13226_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from profiles/traffic_<workload>.txt
+    (key = value lines), or None if absent, for another kernel, or taken on
+    other kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.lstrip().startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_hash") != kernel_source_hash():
+        return None
+    key = f"bytes_per_launch.{kernel}"
+    return int(float(kv[key])) if key in kv else None
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -60,8 +91,9 @@ def parse():
     ap.add_argument("--events", default="inline", choices=["inline", "separate"],
                     help="time groups/kernels with events inside the timed region, or in "
                          "a second pass after a clean one")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file of measured HBM bytes per launch for the dominant kernel")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="before warmup, copy 1 GiB on the device 3 times (a kernel of known "
+                         "traffic that scales FETCH_SIZE / WRITE_SIZE counter runs)")
     return ap.parse_args()
 
 
@@ -176,6 +208,13 @@ def main():
         return [torch.cuda.Event(enable_timing=True) for _ in range(3)]
 
     log(f"workload {desc['workload']}: {len(groups)} groups, H={H} D={D}")
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        del src, dst
     for g in groups:
         g["ev"] = new_events()
     for _ in range(args.warmup):
@@ -259,12 +298,7 @@ def main():
     else:
         achieved = alg[dom] / launches / (kd["avg_ms"] * 1e-3) / 1e12
         roof = dict(bound="mfma", unit="TFLOP/s", peak=BF16_PEAK_TFLOPS)
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            tr = json.load(f)
-        if tr.get("kernel") == dom and tr.get("workload") == desc["workload"]:
-            traffic = tr.get("bytes_per_launch")
+    traffic = measured_traffic(desc["workload"], dom)
     roofline = dict(bound=roof["bound"], kernel=dom, achieved=round(achieved, 2),
                     peak=roof["peak"], unit=roof["unit"], frac=round(achieved / roof["peak"], 4),
                     traffic=traffic, launches=kd["launches"], avg_ms=round(kd["avg_ms"], 5),

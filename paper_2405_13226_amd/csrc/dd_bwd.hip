@@ -117,11 +117,12 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const int grp = wave & 3;
     const bool role_a = wave < 4;
 
-    // Key blocks in ascending order: under the causal mask the first blocks
-    // of a row see the most queries, so the heaviest work starts first.
+    // Slices grouped per XCD; key blocks in ascending order: under the
+    // causal mask the first blocks of a row see the most queries, so the
+    // heaviest work starts first.
     const int BH = B * H;
-    const int kvb = blockIdx.x / BH;
-    const int bh = blockIdx.x % BH;
+    int bh, kvb;
+    block_slice(blockIdx.x, nkb, BH, bh, kvb);
     const int b = bh / H, h = bh % H;
 
     const long long rs = static_cast<long long>(H) * D;
@@ -376,8 +377,8 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
 
     const int BH = B * H;
-    const int kvb = blockIdx.x / BH;
-    const int bh = blockIdx.x % BH;
+    int bh, kvb;
+    block_slice(blockIdx.x, nkb, BH, bh, kvb);
     const int b = bh / H, h = bh % H;
 
     const long long rs = static_cast<long long>(H) * D;
@@ -580,8 +581,9 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
 
     const int BH = B * H;
-    const int qb = nqb - 1 - static_cast<int>(blockIdx.x) / BH;
-    const int bh = blockIdx.x % BH;
+    int bh, jb;
+    block_slice(blockIdx.x, nqb, BH, bh, jb);
+    const int qb = nqb - 1 - jb;
     const int b = bh / H, h = bh % H;
 
     const long long rs = static_cast<long long>(H) * D;

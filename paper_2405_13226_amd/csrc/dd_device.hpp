@@ -1,7 +1,7 @@
 // dd_device.hpp -- device-side building blocks shared by the attention
 // kernels for gfx950 (CDNA4): vector types, the bf16 32x32x16 matrix-core
-// product, bf16 packing, document-span lookup and the tile stager that fills
-// LDS with both row-major and transposed copies of a 4-row x 8-column unit.
+// product, bf16 packing, the mask's document spans, the XCD-aware block map
+// and wave reductions.
 //
 // Matrix-core layout used throughout (v_mfma_f32_32x32x16_bf16, wave64):
 //   A (32 x 16): lane l holds row l%32, k-slots 8*(l/32) .. 8*(l/32)+7
@@ -113,6 +113,26 @@ __device__ __forceinline__ void key_queries(int b, int L, int p, bool causal,
     hi = de - 1;
 }
 
+// Block -> (slice, block-within-slice) map.  Workgroups are dispatched
+// round-robin over the 8 XCDs of the chip (block id % 8); each XCD has its
+// own L2.  When the slice count is a multiple of 8, XCD x receives slices
+// x, x + 8, ..., and all blocks of one slice consecutively, so the blocks
+// that re-read a slice's tiles run together on one L2.  `j` counts the
+// blocks of a slice in dispatch order (callers map it heaviest-first).
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ void block_slice(int bid, int nblk, int BH, int &bh, int &j)
+{
+    if (BH % kXcds == 0) {
+        const int x = bid % kXcds, n = bid / kXcds;
+        bh = (n / nblk) * kXcds + x;
+        j = n % nblk;
+    } else {
+        bh = bid % BH;
+        j = bid / BH;
+    }
+}
+
 // Wave-wide min / max of an int.
 __device__ __forceinline__ int wave_min(int v)
 {
@@ -127,64 +147,6 @@ __device__ __forceinline__ int wave_max(int v)
     for (int o = 32; o >= 1; o >>= 1)
         v = max(v, __shfl_xor(v, o));
     return v;
-}
-
-// ---------------------------------------------------------------------------
-// Tile staging.  A tile is ROWS consecutive token rows x D columns of one
-// (b, h) slice of a [B, L, H, D] bf16 tensor.  The unit of work of a thread is
-// 4 rows x 8 columns (four 16-byte global loads).  A unit can be written to
-// LDS row-major (pitch RP elements, one 16-byte store per row) and/or
-// transposed (column-major with pitch TP elements: column c of the unit is
-// one 8-byte store of the 4 rows).  Rows at or beyond L load as zeros.
-// ---------------------------------------------------------------------------
-struct Unit4x8 {
-    u32x4 r[4];
-};
-
-template <int D>
-__device__ __forceinline__ void load_unit(Unit4x8 &u, const uint16_t *__restrict__ base,
-                                          long long row_stride, int row0, int L, int unit)
-{
-    constexpr int CG = D / 8;  // 8-column groups per row
-    const int rg = unit / CG, cg = unit % CG;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int row = row0 + rg * 4 + i;
-        if (row < L)
-            u.r[i] = *reinterpret_cast<const u32x4 *>(base + row * row_stride + cg * 8);
-        else
-            u.r[i] = u32x4{0u, 0u, 0u, 0u};
-    }
-}
-
-template <int D, int RP>
-__device__ __forceinline__ void store_unit_rows(const Unit4x8 &u, uint16_t *lds, int unit)
-{
-    constexpr int CG = D / 8;
-    const int rg = unit / CG, cg = unit % CG;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        *reinterpret_cast<u32x4 *>(lds + (rg * 4 + i) * RP + cg * 8) = u.r[i];
-}
-
-template <int D, int TP>
-__device__ __forceinline__ void store_unit_cols(const Unit4x8 &u, uint16_t *lds, int unit)
-{
-    constexpr int CG = D / 8;
-    const int rg = unit / CG, cg = unit % CG;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-        const int w = c >> 1;
-        uint32_t lo, hi;
-        if ((c & 1) == 0) {
-            lo = (u.r[0][w] & 0xffffu) | (u.r[1][w] << 16);
-            hi = (u.r[2][w] & 0xffffu) | (u.r[3][w] << 16);
-        } else {
-            lo = (u.r[0][w] >> 16) | (u.r[1][w] & 0xffff0000u);
-            hi = (u.r[2][w] >> 16) | (u.r[3][w] & 0xffff0000u);
-        }
-        *reinterpret_cast<u32x2 *>(lds + (cg * 8 + c) * TP + rg * 4) = u32x2{lo, hi};
-    }
 }
 
 }  // namespace dd

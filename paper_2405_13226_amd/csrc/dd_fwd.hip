@@ -60,11 +60,11 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
 
-    // Heaviest query blocks first: block id -> (query block, b*H + h).
+    // Slices grouped per XCD, heaviest query blocks (the last) first.
     const int BH = B * H;
-    const int bid = blockIdx.x;
-    const int qb = nqb - 1 - bid / BH;
-    const int bh = bid % BH;
+    int bh, jb;
+    block_slice(blockIdx.x, nqb, BH, bh, jb);
+    const int qb = nqb - 1 - jb;
     const int b = bh / H, h = bh % H;
 
     const long long rs = static_cast<long long>(H) * D;  // token stride
