@@ -13,6 +13,8 @@ Workloads (``--workload``):
                  launch per bucket), and the same DD pieces packed into one
                  document-masked launch
   stream         64 steps with L drawn from 256 .. 16384, weights 1/L, D = 128
+  curriculum     48 steps of the length curriculum of Algorithm 1 ("Grow-P2"
+                 odds, 8 cycles, equal tokens from buckets 256 .. 8192), D = 128
   tiny           B = 4, L = 256, H = 4, D = 64
 
 Prints ONE JSON line on stdout: the metric is useful attention TFLOP/s
@@ -81,7 +83,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dd_sweep_d64",
-                    choices=["dd_sweep_d64", "dd_sweep_d128", "chunk_vs_dd", "stream", "tiny"])
+                    choices=["dd_sweep_d64", "dd_sweep_d128", "chunk_vs_dd", "stream",
+                             "curriculum", "tiny"])
     ap.add_argument("--buckets", default=None,
                     help="comma-separated subset of bucket lengths (sweeps only)")
     ap.add_argument("--seed", type=int, default=0)
@@ -132,6 +135,20 @@ def workload(name, seed, buckets=None):
                                            if g.get("variant") == "dd")),
                     note="one bench step runs every variant once; compare the variants' "
                          "ms (dense, masked, the sum of the dd buckets, dd_packed)")
+    elif name == "curriculum":
+        from paper_2405_13226_amd import sampler
+        H, D, cycles = 16, 128, 8
+        lens_all = list(sampler.CURRICULUM_LENGTHS)
+        n = {L: cycles * TOKENS for L in lens_all}            # one step per bucket per cycle
+        rows = {L: n[L] // L for L in lens_all}
+        steps = sampler.curriculum_steps(rows, n, sampler.preset_odds("grow_p2"), cycles, TOKENS,
+                                         np.random.default_rng(seed))
+        lens = [st.length for st in steps]
+        groups = [dict(name=f"step{i} L={L}", B=TOKENS // L, L=L, cu=None)
+                  for i, L in enumerate(lens)]
+        desc = dict(workload=name, tokens_per_group=TOKENS, steps_per_stream=len(lens), H=H,
+                    D=D, causal=True, odds="grow_p2", cycles=cycles,
+                    order=[int(L) for L in lens])
     else:  # stream
         H, D = 16, 128
         lens = synth.length_stream(seed, steps=64)
