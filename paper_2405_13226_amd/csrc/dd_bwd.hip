@@ -656,50 +656,60 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const uint16_t *ks = lds + BUF * T::STAGE;
         const uint16_t *vs = ks + T::TILE;
 
-        // S^T = K Q^T and dP^T = V dO^T (column = this lane's query).
-        f32x16 s[2], dp[2];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            s[kb] = f32x16{};
-            dp[kb] = f32x16{};
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-                const int off = kb * 32 * D + roff[kk];
-                s[kb] = mfma32(lds_row8(ks + off), qf[kk], s[kb]);
-                dp[kb] = mfma32(lds_row8(vs + off), dof[kk], dp[kb]);
-            }
-        }
+        // Per 32-key block: S^T = K Q^T and dP^T = V dO^T (column = this
+        // lane's query), dS^T, then dQ^T += K^T dS^T with K^T read transposed.
+        // Blocks are processed one after the other so that only one block's
+        // scores are live, which leaves registers for LDS reads in flight.
         const int lo_r = lo_q - j0 - 4 * g, hi_r = hi_q - j0 - 4 * g;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb) {
+            // The A fragments are read in batches of KB_STEP k-steps before
+            // their products, so several LDS reads are in flight at once.
+            constexpr int KB_STEP = KK >= 8 ? 4 : KK;
+            f32x16 s = f32x16{}, dp = f32x16{};
+#pragma unroll
+            for (int k0 = 0; k0 < KK; k0 += KB_STEP) {
+                bf16x8 ka[KB_STEP], va[KB_STEP];
+#pragma unroll
+                for (int i = 0; i < KB_STEP; ++i) {
+                    const int off = kb * 32 * D + roff[k0 + i];
+                    ka[i] = lds_row8(ks + off);
+                    va[i] = lds_row8(vs + off);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < KB_STEP; ++i) {
+                    s = mfma32(ka[i], qf[k0 + i], s);
+                    dp = mfma32(va[i], dof[k0 + i], dp);
+                }
+            }
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                float p = fast_exp2(fmaf(s[kb][r], scale_log2, neg_lse2));
+                float p = fast_exp2(fmaf(s[r], scale_log2, neg_lse2));
                 if constexpr (MASKED) {
                     const int kr = kb * 32 + 8 * (r >> 2) + (r & 3);
                     const bool ok = (kr >= lo_r) & (kr <= hi_r);
                     p = ok ? p : 0.f;
                 }
-                dp[kb][r] = p * (dp[kb][r] - my_delta);
+                dp[r] = p * (dp[r] - my_delta);
             }
-
-        // dQ^T += K^T dS^T, K^T read transposed from the K tile.
-        bf16x8 sb[2][2];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int t2 = 0; t2 < 2; ++t2)
-                sb[kb][t2] = pack8(dp[kb], 8 * t2);
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            bf16x8 kt[2][DB];
 #pragma unroll
             for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
                     const uint16_t *kr = ks + (kb * 32 + 16 * t2) * D;
-                    const bf16x8 a = join(lds_tr4(kr + toff[db][0]), lds_tr4(kr + toff[db][1]));
-                    dq[db] = mfma32(a, sb[kb][t2], dq[db]);
+                    kt[t2][db] = join(lds_tr4(kr + toff[db][0]), lds_tr4(kr + toff[db][1]));
                 }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2) {
+                const bf16x8 sb = pack8(dp, 8 * t2);
+#pragma unroll
+                for (int db = 0; db < DB; ++db)
+                    dq[db] = mfma32(kt[t2][db], sb, dq[db]);
+            }
+        }
     };
 
     auto compute = [&](int t, auto bufc) {
