@@ -15,6 +15,9 @@ Workloads (``--workload``):
   stream         64 steps with L drawn from 256 .. 16384, weights 1/L, D = 128
   curriculum     48 steps of the length curriculum of Algorithm 1 ("Grow-P2"
                  odds, 8 cycles, equal tokens from buckets 256 .. 8192), D = 128
+  rope_d128      dd_sweep_d128 with rotary position embedding (base 100,000):
+                 q and k rotated before the forward, dq and dk rotated back in
+                 the backward kernels
   tiny           B = 4, L = 256, H = 4, D = 64
 
 Prints ONE JSON line on stdout: the metric is useful attention TFLOP/s
@@ -35,6 +38,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+ROPE_BASE = 100000.0
 TOKENS = 65536
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
@@ -84,7 +88,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dd_sweep_d64",
                     choices=["dd_sweep_d64", "dd_sweep_d128", "chunk_vs_dd", "stream",
-                             "curriculum", "tiny"])
+                             "curriculum", "rope_d128", "tiny"])
     ap.add_argument("--buckets", default=None,
                     help="comma-separated subset of bucket lengths (sweeps only)")
     ap.add_argument("--seed", type=int, default=0)
@@ -114,6 +118,17 @@ def workload(name, seed, buckets=None):
         groups = [dict(name=f"L={L}", B=TOKENS // L, L=L, cu=None) for L in lens]
         desc = dict(workload=name, tokens_per_group=TOKENS, buckets=lens, H=H, D=D,
                     causal=True)
+    elif name == "rope_d128":
+        # The D=128 sweep with rotary position embedding (base 100,000, the
+        # paper's curriculum runs): the forward rotates q and k (two dd_rope
+        # launches) before attention; the backward rotates dq and dk back in
+        # its kernels' epilogues (dd_attn_bwd_rope).
+        H, D = 16, 128
+        lens = buckets or BUCKETS
+        groups = [dict(name=f"L={L}", B=TOKENS // L, L=L, cu=None, rope=ROPE_BASE)
+                  for L in lens]
+        desc = dict(workload=name, tokens_per_group=TOKENS, buckets=lens, H=H, D=D,
+                    causal=True, rope_base=ROPE_BASE)
     elif name == "tiny":
         H, D = 4, 64
         groups = [dict(name="L=256", B=4, L=256, cu=None)]
@@ -196,6 +211,9 @@ def main():
                    .to(torch.bfloat16) for _ in range(4))
     o = torch.empty_like(q)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    use_rope = any(g.get("rope") for g in groups)
+    qr = torch.empty_like(q) if use_rope else q
+    kr = torch.empty_like(q) if use_rope else k
     lse = torch.empty((ntok, H), dtype=torch.float32, device=dev)
     ws_bytes = max(ddlib.workspace_bytes(g["B"], g["L"], H, D) for g in groups)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
@@ -203,7 +221,7 @@ def main():
         g["docs"] = ddlib.DocLens(g["cu"], g["tokens"], dev) if g["cu"] is not None else None
     P = ctypes.c_void_p
     ptr = {n: P(t.data_ptr()) for n, t in dict(q=q, k=k, v=v, do=do, o=o, dq=dq, dk=dk, dv=dv,
-                                                lse=lse, ws=ws).items()}
+                                                lse=lse, ws=ws, qr=qr, kr=kr).items()}
     stream = torch.cuda.current_stream(dev)
     sptr = P(stream.cuda_stream)
 
@@ -211,15 +229,26 @@ def main():
         B, L = g["B"], g["L"]
         cu = P(g["docs"].dev.data_ptr()) if g["docs"] else None
         nd = g["docs"].n_docs if g["docs"] else 0
-        st = lib.dd_attn_fwd(ptr["q"], ptr["k"], ptr["v"], ptr["o"], ptr["lse"], B, L, H, D, 1,
-                             cu, nd, sptr)
+        base = g.get("rope")
+        if base:
+            for src, dst in (("q", "qr"), ("k", "kr")):
+                st = lib.dd_rope(ptr[src], ptr[dst], B, L, H, D, base, 0, cu, nd, 0, sptr)
+                _lib.check(st, "dd_rope")
+        st = lib.dd_attn_fwd(ptr["qr"], ptr["kr"], ptr["v"], ptr["o"], ptr["lse"], B, L, H, D,
+                             1, cu, nd, sptr)
         _lib.check(st, "dd_attn_fwd")
         if mark:
             g["ev"][1].record(stream)
-        st = lib.dd_attn_bwd(ptr["q"], ptr["k"], ptr["v"], ptr["o"], ptr["do"], ptr["lse"],
-                             ptr["dq"], ptr["dk"], ptr["dv"], B, L, H, D, 1, cu, nd,
-                             ptr["ws"], ws_bytes, sptr)
-        _lib.check(st, "dd_attn_bwd")
+        if base:
+            st = lib.dd_attn_bwd_rope(ptr["qr"], ptr["kr"], ptr["v"], ptr["o"], ptr["do"],
+                                      ptr["lse"], ptr["dq"], ptr["dk"], ptr["dv"], B, L, H, D, 1,
+                                      cu, nd, base, 0, ptr["ws"], ws_bytes, sptr)
+            _lib.check(st, "dd_attn_bwd_rope")
+        else:
+            st = lib.dd_attn_bwd(ptr["qr"], ptr["kr"], ptr["v"], ptr["o"], ptr["do"], ptr["lse"],
+                                 ptr["dq"], ptr["dk"], ptr["dv"], B, L, H, D, 1, cu, nd,
+                                 ptr["ws"], ws_bytes, sptr)
+            _lib.check(st, "dd_attn_bwd")
 
     def new_events():
         return [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -306,10 +335,13 @@ def main():
            for name in per_pair}
     alg["backward_prep"] = sum(2 * g["tokens"] * H * D * 2 + g["tokens"] * H * 12
                                for g in groups) * args.steps
+    # rope: each launch reads and writes one [tokens, H, D] bf16 tensor
+    alg["rope"] = sum(2 * 2 * g["tokens"] * H * D * 2 for g in groups if g.get("rope")) \
+        * args.steps
     dom = max(kern, key=lambda n: kern[n]["total_ms"])
     kd = kern[dom]
     launches = max(kd["launches"], 1)
-    if dom == "backward_prep":
+    if dom in ("backward_prep", "rope"):
         achieved = alg[dom] / launches / (kd["avg_ms"] * 1e-3) / 1e9
         roof = dict(bound="hbm", unit="GB/s", peak=HBM_PEAK_GBS)
     else:
@@ -355,9 +387,14 @@ def cpu_baseline(groups, desc, args):
 
     def run(pairs):
         t = time.perf_counter()
-        oracle.attn_fwd(x["q"], x["k"], x["v"], causal=True, cu_doclens=g["cu"], bh=pairs)
-        oracle.attn_bwd(x["q"], x["k"], x["v"], x["do"], causal=True, cu_doclens=g["cu"],
-                        bh=pairs)
+        if g.get("rope"):
+            from oracle import rope as orope
+            orope.attn_fwd(x["q"], x["k"], x["v"], g["rope"], True, g["cu"], bh=pairs)
+            orope.attn_bwd(x["q"], x["k"], x["v"], x["do"], g["rope"], True, g["cu"], bh=pairs)
+        else:
+            oracle.attn_fwd(x["q"], x["k"], x["v"], causal=True, cu_doclens=g["cu"], bh=pairs)
+            oracle.attn_bwd(x["q"], x["k"], x["v"], x["do"], causal=True, cu_doclens=g["cu"],
+                            bh=pairs)
         return time.perf_counter() - t
 
     all_pairs = [(b, h) for b in range(B) for h in range(H)]

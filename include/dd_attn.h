@@ -96,6 +96,39 @@ int dd_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
                 const int32_t *cu_doclens, int n_docs,
                 void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Rotary position embedding (Sec. 3, "Positional encoding"): the paper
+ * rotates queries and keys before attention with base frequency f_b (10,000,
+ * or 100,000).  Y = R X for one bf16 [B, L, H, D] tensor: components (2j, 2j+1)
+ * of every head vector are rotated by the angle pos * base^(-2j/D); inverse
+ * != 0 applies the transposed rotation (angle negated).  pos is the token's
+ * index in its row, or, with doc_positions != 0 and cu_doclens given, its
+ * index from the start of its document inside the row (every document then
+ * starts at position 0, like a DD sequence).  Angles are formed in double
+ * precision and reduced to [-pi, pi] before an fp32 sine and cosine; Y is
+ * rounded to bf16.  X == Y (in place) is allowed; otherwise X and Y must not
+ * overlap.  base must be finite and > 0.  cu_doclens as for dd_attn_fwd.
+ * Returns a dd_status.
+ */
+int dd_rope(const void *X, void *Y, int B, int L, int H, int D, float base, int inverse,
+            const int32_t *cu_doclens, int n_docs, int doc_positions, void *stream);
+
+/*
+ * Backward for attention over rotated queries and keys.  Q and K are the
+ * rotated tensors the forward consumed (dd_rope of the raw q and k with the
+ * same base, cu_doclens and doc_positions); every other argument is as for
+ * dd_attn_bwd.  dQ and dK are the gradients with respect to the unrotated q
+ * and k: the kernels apply the transposed rotation to their fp32 accumulators
+ * before rounding to bf16.  Returns a dd_status (DD_ERR_SHAPE for a base
+ * that is not finite and > 0).
+ */
+int dd_attn_bwd_rope(const void *Q, const void *K, const void *V, const void *O,
+                     const void *dO, const float *LSE, void *dQ, void *dK, void *dV,
+                     int B, int L, int H, int D, int causal,
+                     const int32_t *cu_doclens, int n_docs, float rope_base,
+                     int doc_positions, void *workspace, size_t workspace_bytes,
+                     void *stream);
+
 /* Workspace bytes dd_attn_bwd needs for this shape (0 for an invalid shape). */
 size_t dd_attn_bwd_workspace_bytes(int B, int L, int H, int D);
 
@@ -122,7 +155,7 @@ const char *dd_status_str(int status);
  * dd_prof_read(kernel, &total_ms, &launches) waits for the recorded events
  * of that kernel and returns the sum of their elapsed times and the number of
  * launches; kernel ids are 0 forward, 1 backward preprocess (delta and
- * log2-LSE), 2 backward dK/dV, 3 backward dQ.  Returns DD_OK, DD_ERR_NULL for
+ * log2-LSE), 2 backward dK/dV, 3 backward dQ, 4 rotary embedding.  Returns DD_OK, DD_ERR_NULL for
  * a NULL output pointer, DD_ERR_SHAPE for an unknown kernel id, or
  * DD_ERR_HIP if the runtime fails.  These calls are serialised internally.
  */

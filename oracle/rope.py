@@ -20,6 +20,11 @@ Positions (the paper is silent; reading): a token's index within its row (the
 DD sequence, or the concat-and-chunk chunk), or with ``doc_positions`` its
 index from the start of its document inside the row, so that every DD piece
 and every document of a masked chunk starts at position 0.
+
+Precision (the paper is silent; reading): the rotated q and k are bf16
+tensors, as a bf16 training step materialises them, i.e. the exact rotation
+rounded to the nearest bf16 (ties to even) before attention; with
+``round_rotated=False`` they stay exact.  Everything else is float64.
 """
 from __future__ import annotations
 
@@ -35,6 +40,14 @@ def widen(x) -> np.ndarray:
     if x.dtype == np.uint16:
         return (x.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     return x.astype(np.float64)
+
+
+def round_bf16(x) -> np.ndarray:
+    """Round float64 values to the nearest bf16 (8 significant bits, ties to
+    even), returned as float64.  Finite, normal-range inputs."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)                      # x = m * 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.round(np.ldexp(m, 8)), e - 8)  # np.round: half to even
 
 
 def positions(B: int, L: int, cu_doclens=None, doc_positions: bool = False) -> np.ndarray:
@@ -72,12 +85,18 @@ def rotate(x, ang, inverse: bool = False) -> np.ndarray:
 
 
 def rope(x, base: float, cu_doclens=None, doc_positions: bool = False,
-         inverse: bool = False) -> np.ndarray:
-    """RoPE of a [B, L, H, D] tensor (bf16 bits or float), float64 result."""
-    x = widen(x)
-    B, L, H, D = x.shape
+         inverse: bool = False, rows=None) -> np.ndarray:
+    """RoPE of a [B, L, H, D] tensor (bf16 bits or float), float64 result.
+    With ``rows`` (batch indices) only those rows are rotated; the others are
+    left zero (for oracles that read only some rows)."""
+    B, L, H, D = np.asarray(x).shape
     ang = angles(positions(B, L, cu_doclens, doc_positions), D, base)  # [B, L, D/2]
-    return rotate(x, ang[:, :, None, :], inverse)
+    if rows is None:
+        return rotate(widen(x), ang[:, :, None, :], inverse)
+    y = np.zeros((B, L, H, D), dtype=np.float64)
+    for b in sorted(set(int(r) for r in rows)):
+        y[b] = rotate(widen(np.asarray(x)[b]), ang[b][:, None, :], inverse)
+    return y
 
 
 def _pairs(bh, B, H):
@@ -86,25 +105,48 @@ def _pairs(bh, B, H):
     return [tuple(p) for p in bh]
 
 
+def _rotated(x, base, cu_doclens, doc_positions, round_rotated, rows=None):
+    y = rope(x, base, cu_doclens, doc_positions, rows=rows)
+    return round_bf16(y) if round_rotated else y
+
+
+def _rows(bh):
+    return None if bh is None else [p[0] for p in bh]
+
+
+def _widen_rows(x, rows):
+    if rows is None:
+        return widen(x)
+    x = np.asarray(x)
+    y = np.zeros(x.shape, dtype=np.float64)
+    for b in sorted(set(rows)):
+        y[b] = widen(x[b])
+    return y
+
+
 def attn_fwd(q, k, v, base: float, causal: bool = True, cu_doclens=None,
-             doc_positions: bool = False, bh=None):
+             doc_positions: bool = False, bh=None, round_rotated: bool = True):
     """Attention over rotated q and k.  Returns (o, lse), each [n_bh, L(, D)]."""
-    qr = rope(q, base, cu_doclens, doc_positions)
-    kr = rope(k, base, cu_doclens, doc_positions)
-    return _attn_fwd(qr, kr, widen(v), causal, cu_doclens, bh)
+    rows = _rows(bh)
+    qr = _rotated(q, base, cu_doclens, doc_positions, round_rotated, rows)
+    kr = _rotated(k, base, cu_doclens, doc_positions, round_rotated, rows)
+    return _attn_fwd(qr, kr, _widen_rows(v, rows), causal, cu_doclens, bh)
 
 
 def attn_bwd(q, k, v, do, base: float, causal: bool = True, cu_doclens=None,
-             doc_positions: bool = False, bh=None):
-    """Gradients of sum(dO * O) with respect to the unrotated q, k and v.
+             doc_positions: bool = False, bh=None, round_rotated: bool = True):
+    """Gradients of sum(dO * O) with respect to the unrotated q, k and v (the
+    rounding of the rotated q, k counts as identity in the chain rule, as the
+    straight-through cast of a bf16 training step does).
 
     Returns (dq, dk, dv), each [n_bh, L, D] in the order of ``bh``.
     """
-    q, k = widen(q), widen(k)
-    B, L, H, D = q.shape
-    qr = rope(q, base, cu_doclens, doc_positions)
-    kr = rope(k, base, cu_doclens, doc_positions)
-    dqr, dkr, dv = _attn_bwd(qr, kr, widen(v), widen(do), causal, cu_doclens, bh)
+    B, L, H, D = np.asarray(q).shape
+    rows = _rows(bh)
+    qr = _rotated(q, base, cu_doclens, doc_positions, round_rotated, rows)
+    kr = _rotated(k, base, cu_doclens, doc_positions, round_rotated, rows)
+    dqr, dkr, dv = _attn_bwd(qr, kr, _widen_rows(v, rows), _widen_rows(do, rows), causal,
+                             cu_doclens, bh)
     ang = angles(positions(B, L, cu_doclens, doc_positions), D, base)  # [B, L, D/2]
     dq = np.empty_like(dqr)
     dk = np.empty_like(dkr)

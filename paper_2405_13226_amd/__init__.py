@@ -11,8 +11,9 @@ include/dd_attn.h.
 """
 from ._lib import DDError, LibraryMissing, lib  # noqa: F401
 from .attention import (DDAttnFunction, DocLens, attention, backward,  # noqa: F401
-                        forward, workspace_bytes)
+                        backward_rope, forward, forward_rope, rope, workspace_bytes)
 from . import dd  # noqa: F401
 
 __all__ = ["forward", "backward", "attention", "DDAttnFunction", "DocLens",
+           "rope", "forward_rope", "backward_rope",
            "workspace_bytes", "lib", "DDError", "LibraryMissing", "dd"]

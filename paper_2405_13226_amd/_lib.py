@@ -17,6 +17,9 @@ SIGNATURES = {
     "dd_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _F, _I, _I, _I, _I, _I, _P, _I, _P]),
     "dd_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _F, _P, _P, _P, _I, _I, _I, _I, _I,
                                    _P, _I, _P, ctypes.c_size_t, _P]),
+    "dd_attn_bwd_rope": (ctypes.c_int, [_P, _P, _P, _P, _P, _F, _P, _P, _P, _I, _I, _I, _I, _I,
+                                        _P, _I, ctypes.c_float, _I, _P, ctypes.c_size_t, _P]),
+    "dd_rope": (ctypes.c_int, [_P, _P, _I, _I, _I, _I, ctypes.c_float, _I, _P, _I, _I, _P]),
     "dd_attn_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I]),
     "dd_doclens_check": (ctypes.c_int, [_P, _I, ctypes.c_longlong]),
     "dd_status_str": (ctypes.c_char_p, [_I]),
@@ -26,7 +29,7 @@ SIGNATURES = {
     "dd_prof_kernel_name": (ctypes.c_char_p, [_I]),
 }
 
-KERNELS = {"forward": 0, "backward_prep": 1, "backward_dkdv": 2, "backward_dq": 3}
+KERNELS = {"forward": 0, "backward_prep": 1, "backward_dkdv": 2, "backward_dq": 3, "rope": 4}
 
 
 def prof_enable(on: bool) -> None:

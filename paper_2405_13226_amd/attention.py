@@ -112,26 +112,91 @@ def backward(q, k, v, o, lse, do, causal: bool = True, cu_doclens=None, workspac
     return dq, dk, dv
 
 
+def rope(x, base: float, cu_doclens=None, doc_positions: bool = False, inverse: bool = False,
+         out=None):
+    """Rotary position embedding of a [B, L, H, D] bf16 tensor (new tensor, or
+    ``out``, which may be ``x`` itself)."""
+    _check_tensor(x, "x")
+    B, L, H, D = x.shape
+    docs = _doclens(cu_doclens, B, L, x.device)
+    y = torch.empty_like(x) if out is None else out
+    if out is not None:
+        _check_tensor(out, "out", x.shape)
+    st = lib().dd_rope(_ptr(x), _ptr(y), B, L, H, D, float(base), int(bool(inverse)),
+                       _ptr(docs.dev) if docs else None, docs.n_docs if docs else 0,
+                       int(bool(doc_positions)), _stream(x.device))
+    check(st, "dd_rope")
+    return y
+
+
+def forward_rope(q, k, v, base: float, causal: bool = True, cu_doclens=None,
+                 doc_positions: bool = False):
+    """Attention over rotated q and k.  Returns (o, lse, q_rot, k_rot); the
+    rotated tensors are what ``backward_rope`` takes."""
+    B, L = q.shape[0], q.shape[1]
+    docs = _doclens(cu_doclens, B, L, q.device)
+    qr = rope(q, base, docs, doc_positions)
+    kr = rope(k, base, docs, doc_positions)
+    o, lse = forward(qr, kr, v, causal, docs)
+    return o, lse, qr, kr
+
+
+def backward_rope(q_rot, k_rot, v, o, lse, do, base: float, causal: bool = True,
+                  cu_doclens=None, doc_positions: bool = False, workspace=None):
+    """Backward of attention over rotated q, k: (dq, dk, dv) with respect to
+    the unrotated q and k (the kernels rotate the gradients back)."""
+    _check_tensor(q_rot, "q_rot")
+    B, L, H, D = q_rot.shape
+    for t, n in ((k_rot, "k_rot"), (v, "v"), (o, "o"), (do, "do")):
+        _check_tensor(t, n, q_rot.shape)
+    _check_tensor(lse, "lse", (B, L, H), torch.float32)
+    docs = _doclens(cu_doclens, B, L, q_rot.device)
+    need = workspace_bytes(B, L, H, D)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q_rot.device)
+    dq, dk, dv = torch.empty_like(q_rot), torch.empty_like(q_rot), torch.empty_like(q_rot)
+    st = lib().dd_attn_bwd_rope(_ptr(q_rot), _ptr(k_rot), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
+                                _ptr(dq), _ptr(dk), _ptr(dv), B, L, H, D, int(bool(causal)),
+                                _ptr(docs.dev) if docs else None, docs.n_docs if docs else 0,
+                                float(base), int(bool(doc_positions)), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(),
+                                _stream(q_rot.device))
+    check(st, "dd_attn_bwd_rope")
+    return dq, dk, dv
+
+
 class DDAttnFunction(torch.autograd.Function):
-    """Autograd wrapper: forward saves (q, k, v, o, lse) for the backward."""
+    """Autograd wrapper: forward saves (q, k, v, o, lse) for the backward, with
+    q and k rotated when a RoPE base is given."""
 
     @staticmethod
-    def forward(ctx, q, k, v, causal, cu_doclens):
+    def forward(ctx, q, k, v, causal, cu_doclens, rope_base, rope_doc_positions):
         B, L = q.shape[0], q.shape[1]
         docs = _doclens(cu_doclens, B, L, q.device)
-        o, lse = forward(q, k, v, causal, docs)
+        if rope_base:
+            o, lse, q, k = forward_rope(q, k, v, rope_base, causal, docs, rope_doc_positions)
+        else:
+            o, lse = forward(q, k, v, causal, docs)
         ctx.save_for_backward(q, k, v, o, lse)
         ctx.causal = causal
         ctx.docs = docs
+        ctx.rope = (rope_base, rope_doc_positions)
         return o
 
     @staticmethod
     def backward(ctx, do):
         q, k, v, o, lse = ctx.saved_tensors
-        dq, dk, dv = backward(q, k, v, o, lse, do.contiguous(), ctx.causal, ctx.docs)
-        return dq, dk, dv, None, None
+        base, docpos = ctx.rope
+        if base:
+            dq, dk, dv = backward_rope(q, k, v, o, lse, do.contiguous(), base, ctx.causal,
+                                       ctx.docs, docpos)
+        else:
+            dq, dk, dv = backward(q, k, v, o, lse, do.contiguous(), ctx.causal, ctx.docs)
+        return dq, dk, dv, None, None, None, None
 
 
-def attention(q, k, v, causal: bool = True, cu_doclens=None):
-    """Differentiable masked causal attention on [B, L, H, D] bf16 tensors."""
-    return DDAttnFunction.apply(q, k, v, causal, cu_doclens)
+def attention(q, k, v, causal: bool = True, cu_doclens=None, rope_base=None,
+              rope_doc_positions: bool = False):
+    """Differentiable masked causal attention on [B, L, H, D] bf16 tensors;
+    with ``rope_base`` the queries and keys are rotated first (RoPE)."""
+    return DDAttnFunction.apply(q, k, v, causal, cu_doclens, rope_base, rope_doc_positions)

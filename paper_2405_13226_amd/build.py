@@ -21,7 +21,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdd_attn.so")
 
 ARCH = "gfx950"
-HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_prof.hip"]
+HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_prof.hip", "dd_rope.hip"]
 CXX_SOURCES = ["dd_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 VALU forms are disabled for all device code.

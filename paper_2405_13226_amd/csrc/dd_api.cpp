@@ -7,6 +7,7 @@
 #include "dd_attn.h"
 #include "dd_internal.h"
 
+#include <cmath>
 #include <cstdint>
 #include <initializer_list>
 
@@ -128,11 +129,12 @@ int dd_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE
     return dd::launch_fwd(a);
 }
 
-int dd_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
-                const void *dO, const float *LSE, void *dQ, void *dK, void *dV,
-                int B, int L, int H, int D, int causal,
-                const int32_t *cu_doclens, int n_docs,
-                void *workspace, size_t workspace_bytes, void *stream)
+namespace {
+
+int attn_bwd_checked(const void *Q, const void *K, const void *V, const void *O, const void *dO,
+                     const float *LSE, void *dQ, void *dK, void *dV, int B, int L, int H, int D,
+                     int causal, const int32_t *cu_doclens, int n_docs, double rope_base,
+                     bool rope_doc, void *workspace, size_t workspace_bytes, void *stream)
 {
     if (!Q || !K || !V || !O || !dO || !LSE || !dQ || !dK || !dV)
         return DD_ERR_NULL;
@@ -169,7 +171,63 @@ int dd_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
     }
     dd::BwdArgs a{Q, K, V, O, dO, LSE, dQ, dK, dV, B, L, H, D, causal != 0,
                   cu_doclens, n_docs, workspace, stream};
+    a.rope_base = rope_base;
+    a.rope_doc = rope_doc;
     return dd::launch_bwd(a);
+}
+
+bool valid_base(float base) { return std::isfinite(base) && base > 0.0f; }
+
+}  // namespace
+
+int dd_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
+                const void *dO, const float *LSE, void *dQ, void *dK, void *dV,
+                int B, int L, int H, int D, int causal,
+                const int32_t *cu_doclens, int n_docs,
+                void *workspace, size_t workspace_bytes, void *stream)
+{
+    return attn_bwd_checked(Q, K, V, O, dO, LSE, dQ, dK, dV, B, L, H, D, causal, cu_doclens,
+                            n_docs, 0.0, false, workspace, workspace_bytes, stream);
+}
+
+int dd_attn_bwd_rope(const void *Q, const void *K, const void *V, const void *O,
+                     const void *dO, const float *LSE, void *dQ, void *dK, void *dV,
+                     int B, int L, int H, int D, int causal,
+                     const int32_t *cu_doclens, int n_docs, float rope_base,
+                     int doc_positions, void *workspace, size_t workspace_bytes,
+                     void *stream)
+{
+    if (!valid_base(rope_base))
+        return DD_ERR_SHAPE;
+    return attn_bwd_checked(Q, K, V, O, dO, LSE, dQ, dK, dV, B, L, H, D, causal, cu_doclens,
+                            n_docs, static_cast<double>(rope_base), doc_positions != 0,
+                            workspace, workspace_bytes, stream);
+}
+
+int dd_rope(const void *X, void *Y, int B, int L, int H, int D, float base, int inverse,
+            const int32_t *cu_doclens, int n_docs, int doc_positions, void *stream)
+{
+    if (!X || !Y)
+        return DD_ERR_NULL;
+    int st = check_shape(B, L, H, D);
+    if (st != DD_OK)
+        return st;
+    if (!valid_base(base))
+        return DD_ERR_SHAPE;
+    st = check_doc_args(cu_doclens, n_docs, B, L);
+    if (st != DD_OK)
+        return st;
+    if (!aligned(X, 16) || !aligned(Y, 16))
+        return DD_ERR_ALIGN;
+    const size_t tb = static_cast<size_t>(B) * L * H * D * 2;
+    Range rx = range_of(X, tb), ry = range_of(Y, tb);
+    if (X != Y && overlaps(rx, ry))
+        return DD_ERR_ALIAS;
+    if (cu_doclens && overlaps(ry, range_of(cu_doclens, static_cast<size_t>(n_docs + 1) * 4)))
+        return DD_ERR_ALIAS;
+    dd::RopeArgs a{X, Y, B, L, H, D, static_cast<double>(base), inverse != 0, cu_doclens,
+                   n_docs, doc_positions != 0, stream};
+    return dd::launch_rope(a);
 }
 
 }  // extern "C"

@@ -25,6 +25,7 @@
 #include "dd_internal.h"
 #include "dd_launch.hpp"
 #include "dd_prof.hpp"
+#include "dd_rope.hpp"
 #include "dd_attn.h"
 
 namespace dd {
@@ -103,7 +104,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             const float *__restrict__ lse2g, const float *__restrict__ deltag,
             uint16_t *__restrict__ dK, uint16_t *__restrict__ dV, int B, int L, int H,
             int causal_i, const int32_t *__restrict__ cu, int n_docs, float scale_log2,
-            float scale, int nkb)
+            float scale, int nkb, RopeEpi rt, int rope)
 {
     using T = KvTile<D>;
     constexpr int KK = D / 16;
@@ -332,6 +333,8 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
     if (!k_ok)
         return;
+    if (!role_a && rope != 0)  // dK with respect to the unrotated keys
+        rope_unrotate_acc<DB>(acc, rt, rope_position(b, L, my_k, cu, n_docs, rope), g);
     const float osc = role_a ? 1.0f : scale;
     uint16_t *dst = (role_a ? dV : dK) + base + my_k * rs;
 #pragma unroll
@@ -365,7 +368,7 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
              const float *__restrict__ lse2g, const float *__restrict__ deltag,
              uint16_t *__restrict__ dK, uint16_t *__restrict__ dV, int B, int L, int H,
              int causal_i, const int32_t *__restrict__ cu, int n_docs, float scale_log2,
-             float scale, int nkb)
+             float scale, int nkb, RopeEpi rt, int rope)
 {
     using T = KvTile1<D>;
     constexpr int KK = D / 16;
@@ -537,6 +540,8 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
     if (!k_ok)
         return;
+    if (rope != 0)  // dK with respect to the unrotated keys
+        rope_unrotate_acc<DB>(dk, rt, rope_position(b, L, my_k, cu, n_docs, rope), g);
     uint16_t *dKb = dK + base + my_k * rs;
     uint16_t *dVb = dV + base + my_k * rs;
 #pragma unroll
@@ -569,7 +574,8 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
           const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
           const float *__restrict__ lse2g, const float *__restrict__ deltag,
           uint16_t *__restrict__ dQ, int B, int L, int H, int causal_i,
-          const int32_t *__restrict__ cu, int n_docs, float scale_log2, float scale, int nqb)
+          const int32_t *__restrict__ cu, int n_docs, float scale_log2, float scale, int nqb,
+          RopeEpi rt, int rope)
 {
     using T = QTile<D>;
     constexpr int KK = D / 16;
@@ -746,6 +752,8 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
     if (!q_ok)
         return;
+    if (rope != 0)  // dQ with respect to the unrotated queries
+        rope_unrotate_acc<DB>(dq, rt, rope_position(b, L, my_q, cu, n_docs, rope), g);
     uint16_t *dQb = dQ + base + my_q * rs;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -765,12 +773,12 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,   \
         const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,      \
         uint16_t *__restrict__, uint16_t *__restrict__, int, int, int, int,                      \
-        const int32_t *__restrict__, int, float, float, int
+        const int32_t *__restrict__, int, float, float, int, RopeEpi, int
 #define DD_Q_ARGS                                                                                \
     const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,   \
         const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,      \
         uint16_t *__restrict__, int, int, int, int, const int32_t *__restrict__, int, float,     \
-        float, int
+        float, int, RopeEpi, int
 #define DD_PREP_ARGS                                                                             \
     const uint16_t *__restrict__, const uint16_t *__restrict__, const float *__restrict__,      \
         float *__restrict__, float *__restrict__, int, int, int
@@ -794,6 +802,9 @@ static int launch_bwd_d(const BwdArgs &a)
     float *delta = reinterpret_cast<float *>(static_cast<char *>(a.workspace) + region);
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
     const float scale_log2 = scale * kLog2e;
+    // RoPE: 0 off, 1 row positions, 2 document-local positions.
+    const int rope = a.rope_base > 0.0 ? (a.rope_doc && a.cu ? 2 : 1) : 0;
+    const RopeEpi rt = rope ? rope_epi(a.rope_base, D) : RopeEpi{};
 
     const long long threads = static_cast<long long>(a.B) * a.L * a.H * (D / 8);
     const unsigned pblocks = static_cast<unsigned>((threads + 255) / 256);
@@ -813,12 +824,12 @@ static int launch_bwd_d(const BwdArgs &a)
             e = launch_kernel(dkdv1_kernel<D>, dim3(static_cast<unsigned>(nkb * a.B * a.H)),
                               dim3(64 * KvTile1<D>::NW), st, a.Q, a.K, a.V, a.dO, lse2, delta,
                               a.dK, a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs,
-                              scale_log2, scale, nkb);
+                              scale_log2, scale, nkb, rt, rope);
         else
             e = launch_kernel(dkdv_kernel<D>, dim3(static_cast<unsigned>(nkb * a.B * a.H)),
                               dim3(64 * KvTile<D>::NW), st, a.Q, a.K, a.V, a.dO, lse2, delta,
                               a.dK, a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs,
-                              scale_log2, scale, nkb);
+                              scale_log2, scale, nkb, rt, rope);
     }
     if (e != hipSuccess)
         return DD_ERR_HIP;
@@ -828,7 +839,7 @@ static int launch_bwd_d(const BwdArgs &a)
         ProfScope prof(K_DQ, st);
         e = launch_kernel(dq_kernel<D>, dim3(static_cast<unsigned>(nqb * a.B * a.H)), dim3(256),
                           st, a.Q, a.K, a.V, a.dO, lse2, delta, a.dQ, a.B, a.L, a.H,
-                          a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, scale, nqb);
+                          a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, scale, nqb, rt, rope);
     }
     return e == hipSuccess ? DD_OK : DD_ERR_HIP;
 }

@@ -29,6 +29,20 @@ struct BwdArgs {
     int n_docs;
     void *workspace;
     void *stream;
+    double rope_base = 0.0;  // > 0: Q and K are rotated; rotate dQ, dK back
+    bool rope_doc = false;   // document-local positions
+};
+
+struct RopeArgs {
+    const void *X;
+    void *Y;
+    int B, L, H, D;
+    double base;
+    bool inverse;
+    const int32_t *cu;
+    int n_docs;
+    bool doc;
+    void *stream;
 };
 
 // Backward scratch: per (b, h) row, LSE in log2 units and delta = rowsum(dO*O),
@@ -42,5 +56,6 @@ inline size_t bwd_workspace_bytes(int B, int L, int H)
 // Both return a dd_status value (DD_OK or DD_ERR_HIP).
 int launch_fwd(const FwdArgs &a);
 int launch_bwd(const BwdArgs &a);
+int launch_rope(const RopeArgs &a);
 
 }  // namespace dd

@@ -5,7 +5,7 @@
 
 namespace dd {
 
-enum KernelId { K_FWD = 0, K_PREP = 1, K_DKDV = 2, K_DQ = 3, K_COUNT = 4 };
+enum KernelId { K_FWD = 0, K_PREP = 1, K_DKDV = 2, K_DQ = 3, K_ROPE = 4, K_COUNT = 5 };
 
 // Brackets one launch: records a start event on `stream` at construction and
 // a stop event at destruction, when timing is enabled (no-op otherwise).

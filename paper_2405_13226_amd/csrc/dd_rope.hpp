@@ -1,0 +1,100 @@
+// dd_rope.hpp -- rotary position embedding on the device (arXiv 2405.13226,
+// Sec. 3, "Positional encoding"): components (2j, 2j+1) of a head vector are
+// rotated by the angle pos * base^(-2j/D).
+//
+// The per-pair frequencies base^(-2j/D) are computed on the host in double
+// precision and passed by value.  An angle pos * theta (up to ~1.6e4 rad) is
+// formed in double and reduced to a fraction of a turn before the fp32 sine
+// and cosine, so its error stays at the fp32 rounding of the reduced angle
+// rather than growing with the position.
+#pragma once
+
+#include "dd_device.hpp"
+
+namespace dd {
+
+constexpr int kMaxHalfD = 64;  // D / 2 for D <= 128
+
+struct RopeTheta {
+    double th[kMaxHalfD];  // base^(-2j/D), j < D/2
+};
+
+// The table for this base and head dimension (host; defined in dd_rope.hip).
+RopeTheta rope_theta(double base, int D);
+
+// Sine and cosine of pos * theta: the angle in turns (a / 2pi) is formed in
+// double and reduced to its fractional part in [-1/2, 1/2]; the hardware
+// sine and cosine take their argument in turns.
+__device__ __forceinline__ void rope_sincos(double theta, int pos, float &s, float &c)
+{
+    const double turns = static_cast<double>(pos) * theta * 0.15915494309189533577;
+    const float t = static_cast<float>(turns - rint(turns));
+    s = __builtin_amdgcn_sinf(t);
+    c = __builtin_amdgcn_cosf(t);
+}
+
+// (x0, x1) rotated by the angle whose sine and cosine are s, c; the transposed
+// rotation when INV.
+template <bool INV>
+__device__ __forceinline__ void rope_pair(float &x0, float &x1, float s, float c)
+{
+    const float y0 = INV ? fmaf(x0, c, x1 * s) : fmaf(x0, c, -x1 * s);
+    const float y1 = INV ? fmaf(x1, c, -x0 * s) : fmaf(x0, s, x1 * c);
+    x0 = y0;
+    x1 = y1;
+}
+
+// Position of row-local token p of row b for mode 1 (row positions) or 2
+// (positions from the start of the token's document inside the row).
+__device__ __forceinline__ int rope_position(int b, int L, int p, const int32_t *__restrict__ cu,
+                                             int n_docs, int mode)
+{
+    if (mode != 2)
+        return p;
+    int ds, de;
+    doc_span(b, L, p, cu, n_docs, ds, de);
+    return p - ds;
+}
+
+// Frequencies for the gradient epilogues, with rho = base^(-2/D):
+// theta_j = p[j] for j < 4, and rho^4, rho^16 to step across the registers
+// of a lane (six doubles instead of the full table keep the kernels' scalar
+// registers free for their main loops).
+struct RopeEpi {
+    double p0, p1, p2, p3, r4, r16;
+};
+
+// (host; defined in dd_rope.hip)
+RopeEpi rope_epi(double base, int D);
+
+// Transposed rotation of the fp32 gradient rows a lane holds in the C layout
+// of a 32x32 product (rows = head dims): acc[db][4*rg + e] is dim
+// db*32 + 8*rg + 4*g + e, so pairs (e, e+1) for e = 0, 2 are in-lane and
+// pair j = 16*db + 4*rg + 2*g + e/2 has theta_j = p[2g + e/2] * r4^rg * r16^db.
+template <int DB>
+__device__ __forceinline__ void rope_unrotate_acc(f32x16 (&acc)[DB], const RopeEpi &re, int pos,
+                                                  int g)
+{
+    const double base0 = g ? re.p2 : re.p0, base1 = g ? re.p3 : re.p1;
+    double step_db = 1.0;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+        double step = step_db;
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+#pragma unroll
+            for (int pe = 0; pe < 2; ++pe) {
+                float s, c;
+                rope_sincos((pe ? base1 : base0) * step, pos, s, c);
+                float x0 = acc[db][4 * rg + 2 * pe], x1 = acc[db][4 * rg + 2 * pe + 1];
+                rope_pair<true>(x0, x1, s, c);
+                acc[db][4 * rg + 2 * pe] = x0;
+                acc[db][4 * rg + 2 * pe + 1] = x1;
+            }
+            step *= re.r4;
+        }
+        step_db *= re.r16;
+    }
+}
+
+}  // namespace dd

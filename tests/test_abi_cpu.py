@@ -139,11 +139,48 @@ def test_bwd_validation(lib):
     assert bwd(lib, cu=fake(7, 64), n_docs=2) == ALIAS
 
 
+def rope_call(lib, x=None, y=None, B=2, L=64, H=2, D=64, base=10000.0, inverse=0, cu=None,
+              n_docs=0, doc=0):
+    return lib.dd_rope(x or fake(0), y or fake(1), B, L, H, D, base, inverse, cu, n_docs, doc, None)
+
+
+def test_rope_validation(lib):
+    assert lib.dd_rope(None, fake(1), 2, 64, 2, 64, 1e4, 0, None, 0, 0, None) == NULL
+    assert lib.dd_rope(fake(0), None, 2, 64, 2, 64, 1e4, 0, None, 0, 0, None) == NULL
+    assert rope_call(lib, B=0) == SHAPE
+    assert rope_call(lib, D=96) == HEADDIM
+    for base in (0.0, -1.0, float("inf"), float("nan")):
+        assert rope_call(lib, base=base) == SHAPE, base
+    assert rope_call(lib, cu=fake(5), n_docs=0) == DOCLENS
+    assert rope_call(lib, x=fake(0, 8)) == ALIGN
+    assert rope_call(lib, y=fake(0, 64)) == ALIAS      # partial overlap of Y with X
+    assert rope_call(lib, y=fake(5), cu=fake(5, 16), n_docs=3) == ALIAS
+
+
+def test_bwd_rope_validation(lib):
+    def call(base=10000.0, **kw):
+        p = [fake(i) for i in range(9)]
+        for i, v in kw.get("ptrs", {}).items():
+            p[i] = v
+        B, L, H, D = 2, 64, 2, 64
+        need = lib.dd_attn_bwd_workspace_bytes(B, L, H, D)
+        return lib.dd_attn_bwd_rope(*p, B, L, H, D, 1, None, 0, base, 0,
+                                    kw.get("ws", fake(9)), kw.get("ws_bytes", need), None)
+    for base in (0.0, -5.0, float("nan"), float("inf")):
+        assert call(base) == SHAPE, base
+    for i in range(9):
+        assert call(ptrs={i: None}) == NULL, i
+    assert call(ws_bytes=10) == WORKSPACE
+    assert call(ptrs={7: fake(6)}) == ALIAS
+
+
 def test_python_wrapper_checks_metadata_on_cpu():
     torch = pytest.importorskip("torch")
     import paper_2405_13226_amd as dd
     q = torch.zeros(1, 4, 1, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         dd.forward(q, q, q)  # CPU tensors are rejected before any call
+    with pytest.raises(ValueError):
+        dd.rope(q, 10000.0)
     with pytest.raises(_lib.DDError):
         dd.DocLens([0, 3, 2, 4], 4, torch.device("cpu"))

@@ -89,7 +89,7 @@ def test_positions():
 
 def _f(q, k, v, do, base, cu, docpos):
     B, L, H, D = q.shape
-    o, _ = R.attn_fwd(q, k, v, base, True, cu, docpos)
+    o, _ = R.attn_fwd(q, k, v, base, True, cu, docpos, round_rotated=False)
     return float((oracle.to_blhd(o, B, H) * do).sum())
 
 
@@ -97,7 +97,8 @@ def _f(q, k, v, do, base, cu, docpos):
 def test_bwd_matches_finite_differences(cu, docpos):
     B, L, H, D, base = 2, 5, 1, 4, 10.0
     q, k, v, do = (rand(B, L, H, D) for _ in range(4))
-    dq, dk, dv = (oracle.to_blhd(x, B, H) for x in R.attn_bwd(q, k, v, do, base, True, cu, docpos))
+    dq, dk, dv = (oracle.to_blhd(x, B, H)
+                  for x in R.attn_bwd(q, k, v, do, base, True, cu, docpos, round_rotated=False))
     eps = 1e-6
     for name, grad in (("q", dq), ("k", dk), ("v", dv)):
         args = {"q": q, "k": k, "v": v}
@@ -120,7 +121,7 @@ def test_rope_changes_attention():
     # a nonzero base frequency must change the result (guards against a no-op rotation)
     q, k, v = (rand(1, 6, 1, 8) for _ in range(3))
     o0, _ = oracle.attn_fwd(q, k, v)
-    o1, _ = R.attn_fwd(q, k, v, 10000.0)
+    o1, _ = R.attn_fwd(q, k, v, 10000.0, round_rotated=False)
     assert np.abs(o1 - o0).max() > 1e-3
     np.testing.assert_allclose(o1[:, 0], o0[:, 0], atol=1e-12)  # row 0 sees only itself
 
@@ -143,6 +144,45 @@ def test_dd_equivalence_with_document_positions():
         np.testing.assert_allclose(lse[sl], oracle.to_blhd(ld, 1, H), atol=1e-12)
         for x, y in zip(g, gd):
             np.testing.assert_allclose(x[sl], oracle.to_blhd(y, 1, H), atol=1e-12)
+
+
+def test_round_bf16_closed_forms():
+    one = 1.0
+    cases = [(one, one), (one + 2.0 ** -8, one),                  # tie -> even (1.0)
+             (one + 3 * 2.0 ** -8, one + 2.0 ** -6),              # tie -> even (odd below)
+             (one + 2.0 ** -8 + 2.0 ** -20, one + 2.0 ** -7),     # just above the tie
+             (-3.0 - 2.0 ** -7, -3.0), (0.1, 0.10009765625), (1000.7, 1000.0)]
+    got = R.round_bf16([c[0] for c in cases])
+    np.testing.assert_array_equal(got, [c[1] for c in cases])
+    # every result is a bf16 value: its float32 bits have 16 zero low bits
+    x = rand(1000) * 100
+    bits = R.round_bf16(x).astype(np.float32).view(np.uint32)
+    assert np.all(bits & 0xFFFF == 0)
+    assert np.all(np.abs(R.round_bf16(x) - x) <= np.abs(x) * 2.0 ** -8)
+
+
+def test_rounding_of_rotated_inputs_is_the_only_difference():
+    q, k, v = (rand(1, 9, 2, 8) for _ in range(3))
+    exact, _ = R.attn_fwd(q, k, v, 10000.0, round_rotated=False)
+    qr = R.round_bf16(R.rope(q, 10000.0))
+    kr = R.round_bf16(R.rope(k, 10000.0))
+    ref, _ = oracle.attn_fwd(qr, kr, v)
+    got, _ = R.attn_fwd(q, k, v, 10000.0)
+    np.testing.assert_array_equal(got, ref)
+    assert np.abs(got - exact).max() < 0.05
+
+
+def test_selected_rows_match_full():
+    q, k, v, do = (rand(3, 10, 2, 8) for _ in range(4))
+    cu = [0, 4, 13, 22, 30]
+    bh = [(2, 1), (0, 0)]
+    full = R.attn_fwd(q, k, v, 10.0, True, cu, True)
+    part = R.attn_fwd(q, k, v, 10.0, True, cu, True, bh=bh)
+    gfull = R.attn_bwd(q, k, v, do, 10.0, True, cu, True)
+    gpart = R.attn_bwd(q, k, v, do, 10.0, True, cu, True, bh=bh)
+    idx = [b * 2 + h for b, h in bh]
+    for a, z in zip(full + gfull, part + gpart):
+        np.testing.assert_array_equal(a[idx], z)
 
 
 def test_widen_bf16_exact():
