@@ -12,6 +12,8 @@ Contents
 * ``metrics``: average sequence length, average context length (Appendix F,
   eq. avg_context) and the count of allowed (query, key) pairs.
 * ``decompose``: the binary dataset decomposition of Sec. 2.1.
+* ``layer``: one OpenLM transformer block (fp64 torch plus the attention
+  oracle), forward and backward.
 * ``rope``: rotary position embedding of queries and keys (Sec. 3,
   "Positional encoding") around the attention definition.
 
@@ -151,4 +153,4 @@ def to_blhd(x, B, H, bh=None):
     return out
 
 
-from . import metrics, decompose, rope  # noqa: E402,F401
+from . import metrics, decompose, rope, layer  # noqa: E402,F401
