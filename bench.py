@@ -18,6 +18,10 @@ Workloads (``--workload``):
   rope_d128      dd_sweep_d128 with rotary position embedding (base 100,000):
                  q and k rotated before the forward, dq and dk rotated back in
                  the backward kernels
+  layer_1b       one OpenLM-1B block (d 2048, 16 heads, SwiGLU 5632, RoPE)
+                 forward + backward per bucket L = 256 .. 8192 at 65,536
+                 tokens: step time, attention's share of it, and the fit
+                 t(L) = alpha + beta * L (value: block TFLOP/s)
   tiny           B = 4, L = 256, H = 4, D = 64
 
 Prints ONE JSON line on stdout: the metric is useful attention TFLOP/s
@@ -88,7 +92,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dd_sweep_d64",
                     choices=["dd_sweep_d64", "dd_sweep_d128", "chunk_vs_dd", "stream",
-                             "curriculum", "rope_d128", "tiny"])
+                             "curriculum", "rope_d128", "layer_1b", "tiny"])
     ap.add_argument("--buckets", default=None,
                     help="comma-separated subset of bucket lengths (sweeps only)")
     ap.add_argument("--seed", type=int, default=0)
@@ -199,6 +203,8 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     buckets = [int(x) for x in args.buckets.split(",")] if args.buckets else None
+    if args.workload == "layer_1b":
+        return run_layer(args, buckets, dev)
     groups, desc = workload(args.workload, args.seed, buckets)
     H, D = desc["H"], desc["D"]
     ntok = max(g["tokens"] for g in groups)
@@ -368,6 +374,81 @@ def main():
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(groups, desc, args)
+    print(json.dumps(result), flush=True)
+
+
+def run_layer(args, buckets, dev):
+    """One OpenLM-1B block fwd+bwd per bucket (torch autograd; attention and RoPE
+    in the library's kernels, projections and MLP as vendor GEMMs)."""
+    import numpy as np
+    import torch
+    from paper_2405_13226_amd import _lib, dd
+    from paper_2405_13226_amd.layer import OPENLM_1B, OpenLMBlock
+
+    d, H, hidden = OPENLM_1B["d"], OPENLM_1B["H"], OPENLM_1B["hidden"]
+    D = d // H
+    lens = buckets or BUCKETS
+    blk = OpenLMBlock(d, H, hidden, ROPE_BASE, device=dev, seed=args.seed)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    x_all = torch.randn((TOKENS, d), generator=gen, device=dev).to(torch.bfloat16)
+    dy_all = torch.randn((TOKENS, d), generator=gen, device=dev).to(torch.bfloat16)
+    attn_kernels = ("forward", "rope", "backward_prep", "backward_dkdv", "backward_dq")
+    log(f"workload layer_1b: d={d} H={H} hidden={hidden} rope_base={ROPE_BASE:g}")
+
+    def step(L):
+        B = TOKENS // L
+        x = x_all.view(B, L, d).detach().requires_grad_(True)
+        blk.zero_grad(set_to_none=True)
+        y = blk(x)
+        y.backward(dy_all.view(B, L, d))
+
+    per = []
+    total_ms = 0.0
+    total_flops = 0.0
+    for L in lens:
+        B = TOKENS // L
+        for _ in range(args.warmup):
+            step(L)
+        torch.cuda.synchronize(dev)
+        _lib.prof_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            step(L)
+        e1.record()
+        torch.cuda.synchronize(dev)
+        _lib.prof_enable(False)
+        ms = e0.elapsed_time(e1) / args.steps
+        attn_ms = sum(_lib.prof_read(_lib.KERNELS[k])[0] for k in attn_kernels) / args.steps
+        gemm = 3 * blk.gemm_flops(TOKENS)
+        af, ab = dd.attention_flops(B, L, H, D, True, None)
+        flops = gemm + af + ab
+        per.append(dict(name=f"L={L}", B=B, L=L, ms=round(ms, 4), attention_ms=round(attn_ms, 4),
+                        attention_share=round(attn_ms / ms, 4),
+                        tflops=round(flops / (ms * 1e-3) / 1e12, 2),
+                        tokens_per_s=round(TOKENS / (ms * 1e-3))))
+        total_ms += ms
+        total_flops += flops
+        log(f"  L={L:5d}  {ms:8.3f} ms  attention {attn_ms:7.3f} ms ({100 * attn_ms / ms:5.1f}%)  "
+            f"{per[-1]['tflops']:7.1f} TFLOP/s")
+    Ls = np.array([g["L"] for g in per], dtype=np.float64)
+    ts = np.array([g["ms"] for g in per])
+    beta, alpha = np.polyfit(Ls, ts, 1)
+    resid = float(np.max(np.abs(alpha + beta * Ls - ts)))
+    log(f"fit t(L) = {alpha:.3f} ms + {beta * 1e3:.4f} us * L (max residual {resid:.3f} ms)")
+    result = {
+        "metric": "OpenLM-1B block fwd+bwd TFLOP/s (GEMM + useful attention FLOPs) at 65,536 tokens/step",
+        "value": round(total_flops / (total_ms * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(total_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 activations, random-init weights)",
+        "config": dict(workload="layer_1b", tokens_per_group=TOKENS, buckets=lens, d=d, H=H,
+                       D=D, hidden=hidden, rope_base=ROPE_BASE, causal=True),
+        "groups": per,
+        "fit": dict(alpha_ms=round(float(alpha), 4), beta_us_per_token=round(float(beta) * 1e3, 5),
+                    max_residual_ms=round(resid, 4)),
+    }
     print(json.dumps(result), flush=True)
 
 
