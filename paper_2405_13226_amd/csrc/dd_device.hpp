@@ -149,4 +149,10 @@ __device__ __forceinline__ int wave_max(int v)
     return v;
 }
 
+// A compile-time int as a type, to select a branch of a generic lambda.
+template <int N>
+struct IC {
+    static constexpr int value = N;
+};
+
 }  // namespace dd

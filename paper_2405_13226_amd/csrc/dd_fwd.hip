@@ -25,11 +25,6 @@
 
 namespace dd {
 
-template <int N>
-struct IC {
-    static constexpr int value = N;
-};
-
 template <int D>
 struct FwdTile {
     static constexpr int BM = 128;            // queries per workgroup
