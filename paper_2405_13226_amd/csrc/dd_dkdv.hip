@@ -8,6 +8,9 @@
 #include "dd_launch.hpp"
 #include "dd_tile.hpp"
 
+#include <algorithm>
+#include <atomic>
+
 namespace dd {
 
 template <int D>
@@ -23,6 +26,73 @@ struct KvTile {
     static constexpr int PBUF_FLOATS = 4 * 64 * 32;
 };
 
+// Instruction classes of __builtin_amdgcn_sched_group_barrier, and how many
+// products' operands are read ahead of the matrix pipe.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
+constexpr int kAhead = 4;
+
+// Work item k of workgroup w among G (G a multiple of 8): the block id that
+// block_slice maps to a (slice, key block), or -1 past the last item.  Each
+// XCD's workgroups (w % 8 = x) take the XCD's block sequence n = 0, 1, ...
+// (block id 8n + x) in rounds of 2C (C = G / 8 workgroups per XCD), in
+// zig-zag order: workgroup c takes positions c and 2C-1-c of every round.
+// Under the causal mask a slice's key blocks cost linearly less work in
+// block order, so each workgroup's pair of a round sums to the same cost.
+__device__ __forceinline__ int kv_item_bid(int k, int w, int G, int n_items)
+{
+    const int x = w % kXcds, c = w / kXcds, C = G / kXcds;
+    const int n = 2 * C * (k >> 1) + ((k & 1) ? 2 * C - 1 - c : c);
+    const int bid = n * kXcds + x;
+    return bid < n_items ? bid : -1;
+}
+
+// A work item: one key block of one (b, h) slice and the query tiles its
+// keys are visible to.
+struct KvItem {
+    int b, bh, kvb, t_begin, t_end;
+    long long base;  // element offset of (b, row 0, h, 0)
+};
+
+template <int D>
+__device__ __forceinline__ KvItem kv_item(int bid, int nkb, int B, int L, int H, bool causal,
+                                          const int32_t *__restrict__ cu, int n_docs)
+{
+    using T = KvTile<D>;
+    KvItem it;
+    block_slice(bid, nkb, B * H, it.bh, it.kvb);
+    it.b = it.bh / H;
+    it.base = (static_cast<long long>(it.b) * L * H + it.bh % H) * D;
+    const int kf0 = it.kvb * T::BN, kl = min(kf0 + T::BN - 1, L - 1);
+    int wlo, whi, tmp;
+    key_queries(it.b, L, kf0, causal, cu, n_docs, wlo, tmp);
+    key_queries(it.b, L, kl, causal, cu, n_docs, tmp, whi);
+    it.t_begin = wlo / T::BM;
+    it.t_end = whi / T::BM;
+    return it;
+}
+
+// Direct-to-LDS loads of query tile t of item x into `stage`: the Q and dO
+// tiles, then lse2 and delta of its rows (waves 0 and 1).
+template <int D>
+__device__ __forceinline__ void kv_issue(const DmaPlan<D, KvTile<D>::BM, KvTile<D>::NW> &plan,
+                                         uint16_t *stage, const uint16_t *__restrict__ Q,
+                                         const uint16_t *__restrict__ dO,
+                                         const float *__restrict__ lse2g,
+                                         const float *__restrict__ deltag, const KvItem &x, int t,
+                                         int L, long long rs, int wave, int lane)
+{
+    using T = KvTile<D>;
+    const int i0 = t * T::BM;
+    plan.issue(stage, Q + x.base, rs, i0, L, wave, lane);
+    plan.issue(stage + T::TILE, dO + x.base, rs, i0, L, wave, lane);
+    float *fs = reinterpret_cast<float *>(stage + 2 * T::TILE);
+    if (wave == 0)
+        dma_row_f32(fs, lse2g + static_cast<long long>(x.bh) * L, i0, L, lane);
+    else if (wave == 1)
+        dma_row_f32(fs + T::BM, deltag + static_cast<long long>(x.bh) * L, i0, L, lane);
+}
+
 // Key-resident dK/dV.  The 32 keys of a group are shared by two waves on the
 // same SIMD (wave w and w + 4):
 //   role A (waves 0-3): K in registers; S = Q K^T, P = exp2(S*c - lse2)
@@ -32,7 +102,15 @@ struct KvTile {
 //                       dK^T += Q^T dS.
 // Each wave holds one accumulator set, so two waves fit per SIMD and one
 // wave's softmax arithmetic overlaps the other's matrix products.
-template <int D>
+//
+// PERSIST = false: one work item per workgroup (grid = all items).
+// PERSIST = true: a workgroup walks its work items (kv_item_bid) back to
+// back.  During the last query tile of an item it already loads the next
+// item's first Q/dO tile into the free LDS stage, and after that tile's
+// mid-tile barrier (when K or V in registers is no longer needed) the next
+// item's K or V rows, so the next item starts without an exposed memory
+// latency.
+template <int D, bool PERSIST>
 __global__ void __launch_bounds__(512, 1)
 dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
@@ -52,53 +130,48 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
     const int grp = wave & 3;
     const bool role_a = wave < 4;
-
-    // Slices grouped per XCD; key blocks in ascending order: under the
-    // causal mask the first blocks of a row see the most queries, so the
-    // heaviest work starts first.
-    const int BH = B * H;
-    int bh, kvb;
-    block_slice(blockIdx.x, nkb, BH, bh, kvb);
-    const int b = bh / H, h = bh % H;
-
     const long long rs = static_cast<long long>(H) * D;
-    const long long base = (static_cast<long long>(b) * L * H + h) * D;
-    const uint16_t *Qb = Q + base, *dOb = dO + base;
-    const float *lse2 = lse2g + static_cast<long long>(bh) * L;
-    const float *dlt = deltag + static_cast<long long>(bh) * L;
+    const int n_items = nkb * B * H;
+    const int G = static_cast<int>(gridDim.x);
 
-    const int k0w = kvb * T::BN + grp * 32;
-    const int my_k = k0w + l32;
-    const bool k_ok = my_k < L;
-    int qlo_k = 1, qhi_k = 0;
-    if (k_ok)
-        key_queries(b, L, my_k, causal, cu, n_docs, qlo_k, qhi_k);
-    const bool wave_on = k0w < L;
-    const int lo_w = wave_min(k_ok ? qlo_k : 0x7fffffff);
-    const int hi_w = wave_max(k_ok ? qhi_k : -1);
-    const int lo_all = wave_max(k_ok ? qlo_k : -1);
-    const int hi_all = wave_min(k_ok ? qhi_k : 0x7fffffff);
-    const bool wave_full_keys = (k0w + 31) < L;
+    int k_item = 0;
+    int bid = kv_item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
+    if (bid < 0)
+        return;
+    KvItem it = kv_item<D>(bid, nkb, B, L, H, causal, cu, n_docs), nit = it;
 
-    const int kf0 = kvb * T::BN, kl = min(kvb * T::BN + T::BN - 1, L - 1);
-    int wlo, whi, tmp;
-    key_queries(b, L, kf0, causal, cu, n_docs, wlo, tmp);
-    key_queries(b, L, kl, causal, cu, n_docs, tmp, whi);
-    const int t_begin = wlo / T::BM, t_end = whi / T::BM;
+    // Per-lane state of the current item.
+    int my_k, qlo_k, qhi_k, lo_w, hi_w, lo_all, hi_all;
+    bool k_ok, wave_on, wave_full_keys;
+    auto setup = [&](const KvItem &x) __attribute__((always_inline)) {
+        const int k0w = x.kvb * T::BN + grp * 32;
+        my_k = k0w + l32;
+        k_ok = my_k < L;
+        qlo_k = 1;
+        qhi_k = 0;
+        if (k_ok)
+            key_queries(x.b, L, my_k, causal, cu, n_docs, qlo_k, qhi_k);
+        wave_on = k0w < L;
+        lo_w = wave_min(k_ok ? qlo_k : 0x7fffffff);
+        hi_w = wave_max(k_ok ? qhi_k : -1);
+        lo_all = wave_max(k_ok ? qlo_k : -1);
+        hi_all = wave_min(k_ok ? qhi_k : 0x7fffffff);
+        wave_full_keys = (k0w + 31) < L;
+    };
 
     // Role A keeps K rows, role B keeps V rows of this lane's key
     // (B operands: column = key).
     bf16x8 kv[KK];
-    {
-        const uint16_t *src = (role_a ? K : V) + base + my_k * rs + g * 8;
+    // A key past L reads row L-1 instead (no branch around the loads, so
+    // they stay in flight until needed): its probabilities are masked to
+    // exactly 0 by a select, and its dK/dV column is never stored.
+    auto load_kv = [&](const KvItem &x) __attribute__((always_inline)) {
+        const int key = min(x.kvb * T::BN + grp * 32 + l32, L - 1);
+        const uint16_t *src = (role_a ? K : V) + x.base + key * rs + g * 8;
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            u32x4 v = u32x4{0u, 0u, 0u, 0u};
-            if (k_ok)
-                v = *reinterpret_cast<const u32x4 *>(src + kk * 16);
-            kv[kk] = as_bf16x8(v);
-        }
-    }
+        for (int kk = 0; kk < KK; ++kk)
+            kv[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(src + kk * 16));
+    };
 
     // Per-lane LDS offsets: row reads (row l32 of a 32-query block, chunk
     // 2*kk + g) and transposed reads (rows 8*hh + 4*g + e of a 16-query step,
@@ -108,37 +181,28 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     for (int kk = 0; kk < KK; ++kk)
         roff[kk] = tile_off<D>(l32, kk * 16 + g * 8);
     {
-        const int G = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
+        const int G16 = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int hh = 0; hh < 2; ++hh)
-                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G & 1) + 4 * c);
+                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G16 & 1) + 4 * c);
     }
     // This lane's slot of the P hand-off buffer: [grp][reg/4][lane][4].
     float *pslot = pbuf + grp * 64 * 32 + lane * 4;
 
     f32x16 acc[DB];  // dV^T (role A) or dK^T (role B)
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-        acc[db] = f32x16{};
 
     DmaPlan<D, T::BM, T::NW> plan;
     plan.init(rs, wave, lane);
-    auto issue = [&](int t, uint16_t *stage) {
-        const int i0 = t * T::BM;
-        plan.issue(stage, Qb, rs, i0, L, wave, lane);
-        plan.issue(stage + T::TILE, dOb, rs, i0, L, wave, lane);
-        float *fs = reinterpret_cast<float *>(stage + 2 * T::TILE);
-        if (wave == 0)
-            dma_row_f32(fs, lse2, i0, L, lane);
-        else if (wave == 1)
-            dma_row_f32(fs + T::BM, dlt, i0, L, lane);
-    };
 
     // Transposed A operand (rows of the 16-query step of (qb, t2)) times a
     // bf16 B operand, accumulated into acc.
+    // Issue order (enforced below): the operands of the first kAhead
+    // products, then one product per pair of reads, so that LDS latency
+    // overlaps the matrix pipe; fenced off from the surrounding code.
     auto tr_products = [&](const uint16_t *tile, const bf16x8 (&bop)[2][2]) {
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
@@ -149,23 +213,42 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     const bf16x8 a = join(lds_tr4(tr + toff[db][0]), lds_tr4(tr + toff[db][1]));
                     acc[db] = mfma32(a, bop[qb][t2], acc[db]);
                 }
+        constexpr int N = 4 * DB;  // products
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * kAhead, 0);
+#pragma unroll
+        for (int i = 0; i < N - kAhead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, kAhead, 0);
+        __builtin_amdgcn_sched_barrier(0);
     };
 
     // Row-wise products X K^T (role A, X = Q) or X V^T (role B, X = dO).
+    // The two 32-query blocks' chains alternate; same issue order as above,
+    // one read per product.
     auto row_products = [&](const uint16_t *tile, f32x16 (&c)[2]) {
+        c[0] = f32x16{};
+        c[1] = f32x16{};
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            c[qb] = f32x16{};
+        for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk)
+            for (int qb = 0; qb < 2; ++qb)
                 c[qb] = mfma32(lds_row8(tile + qb * 32 * D + roff[kk]), kv[kk], c[qb]);
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, kAhead, 0);
+#pragma unroll
+        for (int i = 0; i < 2 * KK - kAhead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
         }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, kAhead, 0);
     };
 
     // Phase 1 of a tile.  Role A: S, P (masked when MASKED), P to LDS and
     // to bf16.  Role B: dP.  Phase 2 (after a barrier): role A dV, role B
-    // dS and dK.
-    auto body = [&](int i0, auto bufc, auto maskc, bool active) {
+    // dS and dK.  With `reload`, every wave loads K or V of the next item
+    // between the phases, where its rows in registers are no longer needed.
+    auto body = [&](int i0, auto bufc, auto maskc, bool active, bool reload) {
         constexpr int BUF = decltype(bufc)::value;
         constexpr bool MASKED = decltype(maskc)::value != 0;
         const uint16_t *qs = lds + BUF * T::STAGE;
@@ -204,13 +287,17 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     for (int t2 = 0; t2 < 2; ++t2)
                         bop[qb][t2] = pack8(c[qb], 8 * t2);
             }
-            __syncthreads();  // P visible to role B
-            if (active)
-                tr_products(dos, bop);  // dV^T += dO^T P
         } else {
             if (active)
                 row_products(dos, c);  // dP
-            __syncthreads();
+        }
+        __syncthreads();  // P visible to role B
+        if (reload)
+            load_kv(nit);
+        if (role_a) {
+            if (active)
+                tr_products(dos, bop);  // dV^T += dO^T P
+        } else {
             if (active) {
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb)
@@ -235,68 +322,157 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
     // The pair of waves of a key group shares one activity decision; every
     // wave reaches the mid-tile barrier.
-    auto compute = [&](int t, auto bufc) {
+    auto compute = [&](int t, auto bufc, bool reload) {
         const int i0 = t * T::BM;
         const bool active = wave_on && i0 <= hi_w && i0 + T::BM - 1 >= lo_w;
         if (wave_full_keys && i0 >= lo_all && i0 + T::BM - 1 <= hi_all)
-            body(i0, bufc, IC<0>{}, active);
+            body(i0, bufc, IC<0>{}, active, reload);
         else
-            body(i0, bufc, IC<1>{}, active);
+            body(i0, bufc, IC<1>{}, active, reload);
     };
 
-    issue(t_begin, lds);
-    wait_vmem();
-    __syncthreads();
-    for (int t = t_begin;;) {
-        if (t < t_end)
-            issue(t + 1, lds + T::STAGE);
-        compute(t, IC<0>{});
-        wait_vmem();
-        __syncthreads();
-        if (t == t_end)
-            break;
-        ++t;
-        if (t < t_end)
-            issue(t + 1, lds);
-        compute(t, IC<1>{});
-        wait_vmem();
-        __syncthreads();
-        if (t == t_end)
-            break;
-        ++t;
-    }
+    // dK (scaled, and with respect to the unrotated keys under RoPE) and dV
+    // of the current item.
+    auto store = [&]() __attribute__((always_inline)) {
+        if (!k_ok)
+            return;
+        if (!role_a && rope != 0) {
+            // Keeps the frequency arithmetic here: hoisted out of the item
+            // loop it would hold ~24 registers across every tile.
+            int gl = g;
+            asm volatile("" : "+v"(gl));
+            rope_unrotate_acc<DB>(acc, rt, rope_position(it.b, L, my_k, cu, n_docs, rope), gl);
+        }
+        const float osc = role_a ? 1.0f : scale;
+        uint16_t *dst = (role_a ? dV : dK) + it.base + my_k * rs;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+                const int d = db * 32 + 8 * rg + 4 * g;
+                *reinterpret_cast<bf16x4 *>(dst + d) =
+                    pack4(acc[db][4 * rg] * osc, acc[db][4 * rg + 1] * osc,
+                          acc[db][4 * rg + 2] * osc, acc[db][4 * rg + 3] * osc);
+            }
+    };
 
-    if (!k_ok)
-        return;
-    if (!role_a && rope != 0)  // dK with respect to the unrotated keys
-        rope_unrotate_acc<DB>(acc, rt, rope_position(b, L, my_k, cu, n_docs, rope), g);
-    const float osc = role_a ? 1.0f : scale;
-    uint16_t *dst = (role_a ? dV : dK) + base + my_k * rs;
+    setup(it);
+    load_kv(it);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-            const int d = db * 32 + 8 * rg + 4 * g;
-            *reinterpret_cast<bf16x4 *>(dst + d) =
-                pack4(acc[db][4 * rg] * osc, acc[db][4 * rg + 1] * osc,
-                      acc[db][4 * rg + 2] * osc, acc[db][4 * rg + 3] * osc);
+        acc[db] = f32x16{};
+    int t = it.t_begin;
+    kv_issue<D>(plan, lds, Q, dO, lse2g, deltag, it, t, L, rs, wave, lane);
+    wait_vmem();
+    __syncthreads();
+
+    // One query tile in LDS stage BUF; the next tile (of this item or the
+    // next one) goes to the other stage.  Returns false after the last item.
+    auto step = [&](auto bufc) __attribute__((always_inline)) -> bool {
+        constexpr int BUF = decltype(bufc)::value;
+        uint16_t *other = lds + (1 - BUF) * T::STAGE;
+        const bool last = t == it.t_end;
+        bool more = false;
+        if (!last) {
+            kv_issue<D>(plan, other, Q, dO, lse2g, deltag, it, t + 1, L, rs, wave, lane);
+        } else if constexpr (PERSIST) {
+            const int nbid = kv_item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
+            more = nbid >= 0;
+            if (more) {
+                nit = kv_item<D>(nbid, nkb, B, L, H, causal, cu, n_docs);
+                kv_issue<D>(plan, other, Q, dO, lse2g, deltag, nit, nit.t_begin, L, rs, wave,
+                                 lane);
+            }
         }
+        compute(t, bufc, more);
+        wait_vmem();
+        __syncthreads();
+        if (!last) {
+            ++t;
+            return true;
+        }
+        store();
+        if (!PERSIST || !more)
+            return false;
+        ++k_item;
+        it = nit;
+        setup(it);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+            acc[db] = f32x16{};
+        t = it.t_begin;
+        return true;
+    };
+    for (;;) {
+        if (!step(IC<0>{}))
+            break;
+        if (!step(IC<1>{}))
+            break;
+    }
 }
 
-template __global__ void dkdv_kernel<128>(
-    const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,
-    const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,
-    uint16_t *__restrict__, uint16_t *__restrict__, int, int, int, int,
-    const int32_t *__restrict__, int, float, float, int, RopeEpi, int);
+#define DD_KV_ARGS                                                                               \
+    const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,   \
+        const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,      \
+        uint16_t *__restrict__, uint16_t *__restrict__, int, int, int, int,                      \
+        const int32_t *__restrict__, int, float, float, int, RopeEpi, int
+template __global__ void dkdv_kernel<128, false>(DD_KV_ARGS);
+template __global__ void dkdv_kernel<128, true>(DD_KV_ARGS);
+#undef DD_KV_ARGS
+
+// Compute units of the current device, cached per device id.
+static int device_cu_count()
+{
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cache[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+        return 0;
+    if (dev < kMaxDevices) {
+        const int v = cache[dev].load(std::memory_order_relaxed);
+        if (v > 0)
+            return v;
+    }
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    if (dev < kMaxDevices)
+        cache[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
+// Below this many tokens per document span (the row, or the mean document
+// length under document masking) a key block visits few query tiles, and
+// the persistent form, which hides each item's set-up behind the previous
+// item, is faster; above it the items are long and one item per workgroup
+// (hardware dispatch) is.
+constexpr long long kPersistMaxSpan = 1024;
 
 hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s)
 {
     using T = KvTile<128>;
     const int nkb = (a.L + T::BN - 1) / T::BN;
-    return launch_kernel(dkdv_kernel<128>, dim3(static_cast<unsigned>(nkb * a.B * a.H)),
-                         dim3(64 * T::NW), static_cast<hipStream_t>(a.stream), a.Q, a.K, a.V,
-                         a.dO, s.lse2, s.delta, a.dK, a.dV, a.B, a.L, a.H, a.causal ? 1 : 0,
-                         a.cu, a.n_docs, s.scale_log2, s.scale, nkb, s.rt, s.rope);
+    const long long n_items = static_cast<long long>(nkb) * a.B * a.H;
+    const long long all = (n_items + kXcds - 1) / kXcds * kXcds;
+    const long long span = a.cu ? std::min<long long>(a.L, static_cast<long long>(a.B) * a.L /
+                                                               std::max(a.n_docs, 1))
+                                : a.L;
+    hipStream_t st = static_cast<hipStream_t>(a.stream);
+    if (span > kPersistMaxSpan)
+        return launch_kernel(dkdv_kernel<128, false>, dim3(static_cast<unsigned>(all)),
+                             dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.delta, a.dK,
+                             a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2,
+                             s.scale, nkb, s.rt, s.rope);
+    // Persistent: at most one workgroup per CU (registers and LDS admit one),
+    // a multiple of the XCD count.
+    const long long cus = device_cu_count();
+    if (cus < kXcds)
+        return hipErrorInvalidDevice;
+    const long long grid = std::min((cus / kXcds) * kXcds, all);
+    return launch_kernel(dkdv_kernel<128, true>, dim3(static_cast<unsigned>(grid)),
+                         dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.delta, a.dK, a.dV,
+                         a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale,
+                         nkb, s.rt, s.rope);
 }
 
 }  // namespace dd

@@ -39,6 +39,26 @@ def test_document_masked_chunks(cuda, D, causal):
     check_case(B, L, H, D, causal=causal, cu=cu, seed=D + causal)
 
 
+# D = 128 spans of <= 1024 tokens take the persistent dK/dV kernel, where a
+# workgroup (one per CU) walks several key blocks back to back.  24 x 3
+# slices of L = 700 make 432 key blocks, so slices 40..71 (b >= 13) have
+# blocks in a workgroup's second item; the last block of every slice holds
+# 60 keys (ragged).  With documents the span is their mean length.
+PERSIST_BH = [(0, 0), (7, 1), (15, 0), (16, 2), (23, 2)]
+
+
+def test_persistent_dkdv_several_items_per_workgroup(cuda):
+    check_case(24, 700, 3, 128, causal=True, seed=11, bh=PERSIST_BH, tag="persistent dK/dV")
+
+
+def test_persistent_dkdv_document_masked(cuda):
+    B, L, H = 24, 700, 3
+    lens = synth.lognormal_doc_lengths(2, total_tokens=B * L, median=300, sigma=0.8)
+    cu = dd.chunk_doclens(lens, B * L)
+    check_case(B, L, H, 128, causal=True, cu=cu, seed=12, bh=PERSIST_BH,
+               tag="persistent dK/dV, documents")
+
+
 def test_single_token_documents(cuda):
     B, L, H, D = 1, 130, 1, 64
     cu = np.arange(0, B * L + 1)

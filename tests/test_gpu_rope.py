@@ -119,6 +119,13 @@ def test_attention_rope_masked_chunks(cuda, D, doc_pos):
     run_rope_attention(B, L, H, D, 10000.0, cu, doc_pos, seed=D)
 
 
+def test_attention_rope_persistent_dkdv(cuda):
+    # 432 ragged key blocks at D = 128: the dK RoPE epilogue runs once per
+    # item inside the persistent dK/dV kernel's item loop.
+    run_rope_attention(24, 700, 3, 128, 100000.0, seed=5,
+                       bh=[(0, 0), (15, 0), (16, 2), (23, 2)])
+
+
 def test_attention_rope_full_bucket_sampled(cuda):
     B, L, H, D = 8, 8192, 16, 128
     run_rope_attention(B, L, H, D, 100000.0, seed=0, bh=[(0, 0), (7, 15), (3, 8)])
