@@ -259,7 +259,21 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         bf16x8 bop[2][2];
         if (role_a) {
             if (active) {
+                // S first: raised issue priority lets role A's products take
+                // the shared matrix pipe ahead of role B's dP, so that dP runs
+                // during A's softmax instead of before it (measured: 3-5%
+                // faster in the persistent form, 1% slower in the other).
+                if constexpr (PERSIST) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    __builtin_amdgcn_s_setprio(3);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
                 row_products(qs, c);
+                if constexpr (PERSIST) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    __builtin_amdgcn_s_setprio(0);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
                 const int qlo_r = qlo_k - i0 - 4 * g, qhi_r = qhi_k - i0 - 4 * g;
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb)
