@@ -66,6 +66,53 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
+class SclkSampler:
+    """Samples the GPU shader clock's current DPM level (sysfs pp_dpm_sclk,
+    the line marked '*') every 10 ms while the timed region runs; summary()
+    is {mean, min, max, samples} in MHz, or None where sysfs is unavailable."""
+
+    def __init__(self, period=0.01):
+        import glob
+        import threading
+        self.paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.period, self.samples = period, []
+        self.stop = threading.Event()
+        self.thread = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        for path in self.paths:
+            try:
+                with open(path) as fh:
+                    for line in fh:
+                        if line.rstrip().endswith("*"):
+                            return float(line.split()[1].lower().rstrip("mhz"))
+            except (OSError, ValueError, IndexError):
+                continue
+        return None
+
+    def _run(self):
+        while not self.stop.wait(self.period):
+            v = self._read()
+            if v is not None:
+                self.samples.append(v)
+
+    def __enter__(self):
+        if self.paths:
+            self.thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self.stop.set()
+        if self.paths:
+            self.thread.join()
+
+    def summary(self):
+        if not self.samples:
+            return None
+        v = self.samples
+        return dict(mean=round(sum(v) / len(v), 1), min=min(v), max=max(v), samples=len(v))
+
+
 def measured_traffic(workload, kernel):
     """HBM bytes per launch of `kernel` from profiles/traffic_<workload>.txt
     (key = value lines), or None if absent, for another kernel, or taken on
@@ -298,7 +345,8 @@ def main():
             _lib.prof_enable(False)
         return wall
 
-    wall = timed(args.events == "inline")
+    with SclkSampler() as sclk:
+        wall = timed(args.events == "inline")
     if args.events == "separate":
         wall_ev = timed(True)
         log(f"wall per step: {wall * 1e3 / args.steps:.3f} ms clean, "
@@ -318,6 +366,7 @@ def main():
         fb, bb = ddlib.dd.attention_bytes(g["B"], g["L"], H, D)
         rec = dict(name=g["name"], B=g["B"], L=g["L"], fwd_ms=round(fm, 4), bwd_ms=round(bm, 4),
                    ms=round(tot, 4), ms_std=round(float(np.std(np.add(f, b))), 4),
+                   ms_median=round(float(np.median(np.add(f, b))), 4),
                    tflops=round((g["flops_fwd"] + g["flops_bwd"]) / (tot * 1e-3) / 1e12, 2),
                    fwd_tflops=round(g["flops_fwd"] / (fm * 1e-3) / 1e12, 2),
                    bwd_tflops=round(g["flops_bwd"] / (bm * 1e-3) / 1e12, 2),
@@ -371,6 +420,7 @@ def main():
         "config": desc,
         "tokens_per_s": round(tokens_step / (ms_per_step * 1e-3)),
         "groups": per_group, "kernels": kern, "roofline": roofline,
+        "sclk_mhz": sclk.summary(),
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(groups, desc, args)
