@@ -33,10 +33,12 @@
  * statistics; probabilities and dS are rounded to bf16 before their products.
  *
  * Ownership.  Every tensor pointer is a DEVICE pointer owned by the caller,
- * including the backward workspace.  The library allocates no device memory,
- * keeps no pointer after a call returns and, apart from the opt-in timing
- * records of dd_prof_enable(), holds no state, so calls are thread-safe.  Work is enqueued asynchronously on `stream` (a hipStream_t;
- * NULL = the default stream); outputs are valid once the caller synchronises.
+ * including the backward workspace.  The library allocates no device memory
+ * and keeps no pointer after a call returns.  Its only state is a per-device
+ * cache of the compute-unit count (filled on first use, atomically) and the
+ * opt-in timing records of dd_prof_enable(), so calls are thread-safe.  Work
+ * is enqueued asynchronously on `stream` (a hipStream_t; NULL = the default
+ * stream); outputs are valid once the caller synchronises.
  *
  * Errors.  Arguments are validated on the host before anything is enqueued;
  * on error nothing is launched and outputs are untouched.  No exception
@@ -155,9 +157,10 @@ const char *dd_status_str(int status);
  * dd_prof_read(kernel, &total_ms, &launches) waits for the recorded events
  * of that kernel and returns the sum of their elapsed times and the number of
  * launches; kernel ids are 0 forward, 1 backward preprocess (delta and
- * log2-LSE), 2 backward dK/dV, 3 backward dQ, 4 rotary embedding.  Returns DD_OK, DD_ERR_NULL for
- * a NULL output pointer, DD_ERR_SHAPE for an unknown kernel id, or
- * DD_ERR_HIP if the runtime fails.  These calls are serialised internally.
+ * log2-LSE), 2 backward dK/dV, 3 backward dQ, 4 rotary embedding.  Returns
+ * DD_OK, DD_ERR_NULL for a NULL output pointer, DD_ERR_SHAPE for an unknown
+ * kernel id, or DD_ERR_HIP if the runtime fails.  These calls are serialised
+ * internally.
  */
 int dd_prof_enable(int on);
 int dd_prof_read(int kernel, double *total_ms, long long *launches);
