@@ -388,15 +388,13 @@ def main():
     per_pair = {"forward": 4, "backward_dkdv": 8, "backward_dq": 2}
     alg = {name: sum(per_pair[name] * D * g["pairs"] for g in groups) * args.steps
            for name in per_pair}
-    alg["backward_prep"] = sum(2 * g["tokens"] * H * D * 2 + g["tokens"] * H * 12
-                               for g in groups) * args.steps
     # rope: each launch reads and writes one [tokens, H, D] bf16 tensor
     alg["rope"] = sum(2 * 2 * g["tokens"] * H * D * 2 for g in groups if g.get("rope")) \
         * args.steps
     dom = max(kern, key=lambda n: kern[n]["total_ms"])
     kd = kern[dom]
     launches = max(kd["launches"], 1)
-    if dom in ("backward_prep", "rope"):
+    if dom == "rope":
         achieved = alg[dom] / launches / (kd["avg_ms"] * 1e-3) / 1e9
         roof = dict(bound="hbm", unit="GB/s", peak=HBM_PEAK_GBS)
     else:
@@ -443,7 +441,7 @@ def run_layer(args, buckets, dev):
     gen.manual_seed(args.seed)
     x_all = torch.randn((TOKENS, d), generator=gen, device=dev).to(torch.bfloat16)
     dy_all = torch.randn((TOKENS, d), generator=gen, device=dev).to(torch.bfloat16)
-    attn_kernels = ("forward", "rope", "backward_prep", "backward_dkdv", "backward_dq")
+    attn_kernels = ("forward", "rope", "backward_dkdv", "backward_dq")
     log(f"workload layer_1b: d={d} H={H} hidden={hidden} rope_base={ROPE_BASE:g}")
 
     def step(L):

@@ -1,9 +1,15 @@
 // dd_bwd.hip -- backward of masked causal attention on gfx950, recomputing
 // the probabilities from the forward's log-sum-exp.
 //
-// Three launches on the caller's stream:
-//   1. prep:  delta_i = sum_d dO_id O_id and LSE in log2 units, both fp32 in
-//             a [B*H][L] workspace (one contiguous row per (b, h)).
+// Two launches on the caller's stream:
+//   1. dq:    query-resident.  One workgroup = 4 waves = 128 queries; each
+//             wave keeps its queries' Q and dO rows in registers.  It first
+//             forms delta_i = sum_d dO_id O_id and the LSE in log2 units for
+//             its queries and writes both, fp32, to a [B*H][L] workspace (one
+//             contiguous row per (b, h)); then it walks the key tiles (64
+//             keys) its queries see and forms
+//               S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T,
+//             with K and V tiles in LDS (K^T read transposed).
 //   2. dkdv:  key-resident, 128 keys per workgroup.  For D = 128
 //             (dd_dkdv.hip) the two waves of a 32-key group keep K (one) and
 //             V (the other) rows in registers; for D = 64 (here) one wave
@@ -11,14 +17,10 @@
 //             are visible to and form
 //               S = Q K^T, P = exp2(S*scale*log2e - lse2), dP = dO V^T,
 //               dS = P * (dP - delta),
-//               dV^T += dO^T P,  dK^T += Q^T dS.
+//               dV^T += dO^T P,  dK^T += Q^T dS,
+//             reading lse2 and delta of each tile from the workspace.
 //             Q and dO tiles arrive row-major in LDS by direct DMA; S and dP
 //             read them row-wise, dV^T and dK^T transposed (ds_read_b64_tr_b16).
-//   3. dq:    query-resident.  One workgroup = 4 waves = 128 queries; each
-//             wave keeps its queries' Q and dO rows in registers, walks the
-//             key tiles (64 keys) its queries see and forms
-//               S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T,
-//             with K and V tiles in LDS (K^T read transposed).
 // Splitting dQ from dK/dV keeps every output owned by exactly one workgroup:
 // no atomics, deterministic results, at the cost of recomputing S and dP.
 #include "dd_bwd.hpp"
@@ -30,44 +32,7 @@
 namespace dd {
 
 // ---------------------------------------------------------------------------
-// 1. delta and log2-LSE
-// ---------------------------------------------------------------------------
-template <int D>
-__global__ void __launch_bounds__(256)
-prep_kernel(const uint16_t *__restrict__ O, const uint16_t *__restrict__ dO,
-            const float *__restrict__ LSE, float *__restrict__ lse2, float *__restrict__ delta,
-            int B, int L, int H)
-{
-    constexpr int CG = D / 8;  // lanes per (token, head) row
-    const long long gid = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x;
-    const long long rows = static_cast<long long>(B) * L * H;
-    const long long row = gid / CG;
-    const int cg = static_cast<int>(gid % CG);
-    float acc = 0.f;
-    if (row < rows) {
-        const u32x4 o = *reinterpret_cast<const u32x4 *>(O + row * D + cg * 8);
-        const u32x4 d = *reinterpret_cast<const u32x4 *>(dO + row * D + cg * 8);
-        const bf16x8 ob = as_bf16x8(o), db = as_bf16x8(d);
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            acc += static_cast<float>(ob[i]) * static_cast<float>(db[i]);
-    }
-#pragma unroll
-    for (int off = CG / 2; off >= 1; off >>= 1)
-        acc += __shfl_xor(acc, off);
-    if (row < rows && cg == 0) {
-        const int h = static_cast<int>(row % H);
-        const long long tok = row / H;
-        const int i = static_cast<int>(tok % L);
-        const int b = static_cast<int>(tok / L);
-        const long long w = (static_cast<long long>(b) * H + h) * L + i;
-        delta[w] = acc;
-        lse2[w] = LSE[row] * kLog2e;
-    }
-}
-
-// ---------------------------------------------------------------------------
-// 2. dK, dV
+// 1. dK, dV
 // ---------------------------------------------------------------------------
 
 // Key-resident dK/dV for small head dims: one wave owns the 32 keys of a
@@ -280,7 +245,7 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 }
 
 // ---------------------------------------------------------------------------
-// 3. dQ
+// 2. dQ, delta and log2-LSE
 // ---------------------------------------------------------------------------
 template <int D>
 struct QTile {
@@ -293,8 +258,9 @@ struct QTile {
 template <int D>
 __global__ void __launch_bounds__(256, 2)
 dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
-          const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
-          const float *__restrict__ lse2g, const float *__restrict__ deltag,
+          const uint16_t *__restrict__ V, const uint16_t *__restrict__ O,
+          const uint16_t *__restrict__ dO, const float *__restrict__ LSE,
+          float *__restrict__ lse2g, float *__restrict__ deltag,
           uint16_t *__restrict__ dQ, int B, int L, int H, int causal_i,
           const int32_t *__restrict__ cu, int n_docs, float scale_log2, float scale, int nqb,
           RopeEpi rt, int rope)
@@ -337,20 +303,36 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     query_keys(b, L, ql, causal, cu, n_docs, tmp, whi);
     const int t_begin = wlo / T::BN, t_end = whi / T::BN;
 
+    // Q and dO rows of this lane's query (k-slots 8g..8g+7 of each 16-wide
+    // step), and delta = rowsum(dO * O) from the same slots of O: a partial
+    // per lane, completed with the lane holding the other half of the row.
     bf16x8 qf[KK], dof[KK];
+    float part = 0.f;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-        u32x4 qv = u32x4{0u, 0u, 0u, 0u}, dv = u32x4{0u, 0u, 0u, 0u};
+        u32x4 qv = u32x4{0u, 0u, 0u, 0u}, dv = u32x4{0u, 0u, 0u, 0u}, ov = dv;
         if (q_ok) {
-            qv = *reinterpret_cast<const u32x4 *>(Q + base + my_q * rs + kk * 16 + g * 8);
-            dv = *reinterpret_cast<const u32x4 *>(dO + base + my_q * rs + kk * 16 + g * 8);
+            const long long at = base + my_q * rs + kk * 16 + g * 8;
+            qv = *reinterpret_cast<const u32x4 *>(Q + at);
+            dv = *reinterpret_cast<const u32x4 *>(dO + at);
+            ov = *reinterpret_cast<const u32x4 *>(O + at);
         }
         qf[kk] = as_bf16x8(qv);
         dof[kk] = as_bf16x8(dv);
+        const bf16x8 ob = as_bf16x8(ov);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            part += static_cast<float>(ob[i]) * static_cast<float>(dof[kk][i]);
     }
-    const long long wrow = static_cast<long long>(bh) * L;
-    const float neg_lse2 = q_ok ? -lse2g[wrow + my_q] : 0.f;
-    const float my_delta = q_ok ? deltag[wrow + my_q] : 0.f;
+    const float my_delta = part + __shfl_xor(part, 32);
+    const float lse2 = q_ok ? LSE[(static_cast<long long>(b) * L + my_q) * H + h] * kLog2e : 0.f;
+    const float neg_lse2 = -lse2;
+    // Both, in [B*H][L] rows, for the dK/dV kernel that runs after this one.
+    if (q_ok && g == 0) {
+        const long long wrow = static_cast<long long>(bh) * L;
+        deltag[wrow + my_q] = my_delta;
+        lse2g[wrow + my_q] = lse2;
+    }
 
     int roff[KK], toff[DB][2];
 #pragma unroll
@@ -498,20 +480,14 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const int32_t *__restrict__, int, float, float, int, RopeEpi, int
 #define DD_Q_ARGS                                                                                \
     const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,   \
-        const uint16_t *__restrict__, const float *__restrict__, const float *__restrict__,      \
-        uint16_t *__restrict__, int, int, int, int, const int32_t *__restrict__, int, float,     \
-        float, int, RopeEpi, int
-#define DD_PREP_ARGS                                                                             \
-    const uint16_t *__restrict__, const uint16_t *__restrict__, const float *__restrict__,      \
-        float *__restrict__, float *__restrict__, int, int, int
-template __global__ void prep_kernel<64>(DD_PREP_ARGS);
-template __global__ void prep_kernel<128>(DD_PREP_ARGS);
+        const uint16_t *__restrict__, const uint16_t *__restrict__, const float *__restrict__,   \
+        float *__restrict__, float *__restrict__, uint16_t *__restrict__, int, int, int, int,     \
+        const int32_t *__restrict__, int, float, float, int, RopeEpi, int
 template __global__ void dkdv1_kernel<64>(DD_KV_ARGS);   // D = 64: single-role waves
 template __global__ void dq_kernel<64>(DD_Q_ARGS);
 template __global__ void dq_kernel<128>(DD_Q_ARGS);
 #undef DD_KV_ARGS
 #undef DD_Q_ARGS
-#undef DD_PREP_ARGS
 
 // ---------------------------------------------------------------------------
 template <int D>
@@ -530,13 +506,15 @@ static int launch_bwd_d(const BwdArgs &a)
     s.rope = a.rope_base > 0.0 ? (a.rope_doc && a.cu ? 2 : 1) : 0;
     s.rt = s.rope ? rope_epi(a.rope_base, D) : RopeEpi{};
 
-    const long long threads = static_cast<long long>(a.B) * a.L * a.H * (D / 8);
-    const unsigned pblocks = static_cast<unsigned>((threads + 255) / 256);
+    // dQ first: it also writes delta and log2-LSE, which dK/dV reads.
     hipError_t e;
+    const int nqb = (a.L + QTile<D>::BM - 1) / QTile<D>::BM;
     {
-        ProfScope prof(K_PREP, st);
-        e = launch_kernel(prep_kernel<D>, dim3(pblocks), dim3(256), st, a.O, a.dO, a.LSE, lse2,
-                          delta, a.B, a.L, a.H);
+        ProfScope prof(K_DQ, st);
+        e = launch_kernel(dq_kernel<D>, dim3(static_cast<unsigned>(nqb * a.B * a.H)), dim3(256),
+                          st, a.Q, a.K, a.V, a.O, a.dO, a.LSE, lse2, delta, a.dQ, a.B, a.L, a.H,
+                          a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale, nqb, s.rt,
+                          s.rope);
     }
     if (e != hipSuccess)
         return DD_ERR_HIP;
@@ -552,17 +530,6 @@ static int launch_bwd_d(const BwdArgs &a)
         } else {
             e = launch_dkdv_paired(a, s);
         }
-    }
-    if (e != hipSuccess)
-        return DD_ERR_HIP;
-
-    const int nqb = (a.L + QTile<D>::BM - 1) / QTile<D>::BM;
-    {
-        ProfScope prof(K_DQ, st);
-        e = launch_kernel(dq_kernel<D>, dim3(static_cast<unsigned>(nqb * a.B * a.H)), dim3(256),
-                          st, a.Q, a.K, a.V, a.dO, lse2, delta, a.dQ, a.B, a.L, a.H,
-                          a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale, nqb, s.rt,
-                          s.rope);
     }
     return e == hipSuccess ? DD_OK : DD_ERR_HIP;
 }
