@@ -39,6 +39,12 @@ namespace dd {
 // group with both K and V in registers and both accumulators, and walks the
 // 64-query tile as two 32-query halves to keep its live registers low enough
 // for several waves per SIMD.
+//
+// PERSIST = false: one work item (key block) per workgroup.  PERSIST = true:
+// a workgroup walks its work items (kv_item_bid) back to back; during an
+// item's last query tile it loads the next item's first Q/dO tile into the
+// free LDS stage, and after that tile the next item's K and V rows (holding
+// them during the tile as well would spill at D = 64).
 template <int D>
 struct KvTile1 {
     static constexpr int BN = 128;            // keys per workgroup
@@ -48,7 +54,7 @@ struct KvTile1 {
     static constexpr int STAGE = 2 * TILE + 2 * BM * 2;
 };
 
-template <int D>
+template <int D, bool PERSIST>
 __global__ void __launch_bounds__(256, 2)
 dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
              const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
@@ -65,81 +71,66 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
-
-    const int BH = B * H;
-    int bh, kvb;
-    block_slice(blockIdx.x, nkb, BH, bh, kvb);
-    const int b = bh / H, h = bh % H;
-
     const long long rs = static_cast<long long>(H) * D;
-    const long long base = (static_cast<long long>(b) * L * H + h) * D;
-    const uint16_t *Qb = Q + base, *dOb = dO + base;
-    const float *lse2 = lse2g + static_cast<long long>(bh) * L;
-    const float *dlt = deltag + static_cast<long long>(bh) * L;
+    const int n_items = nkb * B * H;
+    const int G = static_cast<int>(gridDim.x);
 
-    const int k0w = kvb * T::BN + wave * 32;
-    const int my_k = k0w + l32;
-    const bool k_ok = my_k < L;
-    int qlo_k = 1, qhi_k = 0;
-    if (k_ok)
-        key_queries(b, L, my_k, causal, cu, n_docs, qlo_k, qhi_k);
-    const bool wave_on = k0w < L;
-    const int lo_w = wave_min(k_ok ? qlo_k : 0x7fffffff);
-    const int hi_w = wave_max(k_ok ? qhi_k : -1);
-    const int lo_all = wave_max(k_ok ? qlo_k : -1);
-    const int hi_all = wave_min(k_ok ? qhi_k : 0x7fffffff);
-    const bool wave_full_keys = (k0w + 31) < L;
+    int k_item = 0;
+    const int bid = kv_item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
+    if (bid < 0)
+        return;
+    KvItem it = kv_item<D, T>(bid, nkb, B, L, H, causal, cu, n_docs), nit = it;
 
-    const int kf0 = kvb * T::BN, kl = min(kvb * T::BN + T::BN - 1, L - 1);
-    int wlo, whi, tmp;
-    key_queries(b, L, kf0, causal, cu, n_docs, wlo, tmp);
-    key_queries(b, L, kl, causal, cu, n_docs, tmp, whi);
-    const int t_begin = wlo / T::BM, t_end = whi / T::BM;
+    // Per-lane state of the current item.
+    int my_k, qlo_k, qhi_k, lo_w, hi_w, lo_all, hi_all;
+    bool k_ok, wave_on, wave_full_keys;
+    auto setup = [&](const KvItem &x) __attribute__((always_inline)) {
+        const int k0w = x.kvb * T::BN + wave * 32;
+        my_k = k0w + l32;
+        k_ok = my_k < L;
+        qlo_k = 1;
+        qhi_k = 0;
+        if (k_ok)
+            key_queries(x.b, L, my_k, causal, cu, n_docs, qlo_k, qhi_k);
+        wave_on = k0w < L;
+        lo_w = wave_min(k_ok ? qlo_k : 0x7fffffff);
+        hi_w = wave_max(k_ok ? qhi_k : -1);
+        lo_all = wave_max(k_ok ? qlo_k : -1);
+        hi_all = wave_min(k_ok ? qhi_k : 0x7fffffff);
+        wave_full_keys = (k0w + 31) < L;
+    };
 
+    // K and V rows of this lane's key (B operands: column = key).  A key past
+    // L reads row L-1 instead (no branch around the loads, so they stay in
+    // flight until needed): its probabilities are masked to exactly 0 by a
+    // select, and its dK/dV column is never stored.
     bf16x8 kf[KK], vf[KK];
+    auto load_kv = [&](const KvItem &x) __attribute__((always_inline)) {
+        const int key = min(x.kvb * T::BN + wave * 32 + l32, L - 1);
+        const long long at = x.base + key * rs + g * 8;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-        u32x4 kv = u32x4{0u, 0u, 0u, 0u}, vv = u32x4{0u, 0u, 0u, 0u};
-        if (k_ok) {
-            kv = *reinterpret_cast<const u32x4 *>(K + base + my_k * rs + kk * 16 + g * 8);
-            vv = *reinterpret_cast<const u32x4 *>(V + base + my_k * rs + kk * 16 + g * 8);
+        for (int kk = 0; kk < KK; ++kk) {
+            kf[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(K + at + kk * 16));
+            vf[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(V + at + kk * 16));
         }
-        kf[kk] = as_bf16x8(kv);
-        vf[kk] = as_bf16x8(vv);
-    }
+    };
 
     int roff[KK], toff[DB][2];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk)
         roff[kk] = tile_off<D>(l32, kk * 16 + g * 8);
     {
-        const int G = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
+        const int G16 = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int hh = 0; hh < 2; ++hh)
-                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G & 1) + 4 * c);
+                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G16 & 1) + 4 * c);
     }
 
     f32x16 dk[DB], dv[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-        dk[db] = f32x16{};
-        dv[db] = f32x16{};
-    }
-
     DmaPlan<D, T::BM, T::NW> plan;
     plan.init(rs, wave, lane);
-    auto issue = [&](int t, uint16_t *stage) {
-        const int i0 = t * T::BM;
-        plan.issue(stage, Qb, rs, i0, L, wave, lane);
-        plan.issue(stage + T::TILE, dOb, rs, i0, L, wave, lane);
-        float *fs = reinterpret_cast<float *>(stage + 2 * T::TILE);
-        if (wave == 0)
-            dma_row_f32(fs, lse2, i0, L, lane);
-        else if (wave == 1)
-            dma_row_f32(fs + T::BM, dlt, i0, L, lane);
-    };
 
     auto body = [&](int i0, auto bufc, auto maskc) {
         constexpr int BUF = decltype(bufc)::value;
@@ -203,45 +194,92 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             body(i0, bufc, IC<1>{});
     };
 
-    issue(t_begin, lds);
+    // dK (scaled, and with respect to the unrotated keys under RoPE) and dV
+    // of the current item.
+    auto store = [&]() __attribute__((always_inline)) {
+        if (!k_ok)
+            return;
+        if (rope != 0) {
+            // Keeps the frequency arithmetic here: hoisted out of the item
+            // loop it would hold registers across every tile.
+            int gl = g;
+            asm volatile("" : "+v"(gl));
+            rope_unrotate_acc<DB>(dk, rt, rope_position(it.b, L, my_k, cu, n_docs, rope), gl);
+        }
+        uint16_t *dKb = dK + it.base + my_k * rs;
+        uint16_t *dVb = dV + it.base + my_k * rs;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+                const int d = db * 32 + 8 * rg + 4 * g;
+                *reinterpret_cast<bf16x4 *>(dKb + d) =
+                    pack4(dk[db][4 * rg] * scale, dk[db][4 * rg + 1] * scale,
+                          dk[db][4 * rg + 2] * scale, dk[db][4 * rg + 3] * scale);
+                *reinterpret_cast<bf16x4 *>(dVb + d) = pack4(
+                    dv[db][4 * rg], dv[db][4 * rg + 1], dv[db][4 * rg + 2], dv[db][4 * rg + 3]);
+            }
+    };
+
+    setup(it);
+    load_kv(it);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+        dk[db] = f32x16{};
+        dv[db] = f32x16{};
+    }
+    int t = it.t_begin;
+    kv_issue<D, T>(plan, lds, Q, dO, lse2g, deltag, it, t, L, rs, wave, lane);
     wait_vmem();
     __syncthreads();
-    for (int t = t_begin;;) {
-        if (t < t_end)
-            issue(t + 1, lds + T::STAGE);
-        compute(t, IC<0>{});
-        wait_vmem();
-        __syncthreads();
-        if (t == t_end)
-            break;
-        ++t;
-        if (t < t_end)
-            issue(t + 1, lds);
-        compute(t, IC<1>{});
-        wait_vmem();
-        __syncthreads();
-        if (t == t_end)
-            break;
-        ++t;
-    }
 
-    if (!k_ok)
-        return;
-    if (rope != 0)  // dK with respect to the unrotated keys
-        rope_unrotate_acc<DB>(dk, rt, rope_position(b, L, my_k, cu, n_docs, rope), g);
-    uint16_t *dKb = dK + base + my_k * rs;
-    uint16_t *dVb = dV + base + my_k * rs;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-            const int d = db * 32 + 8 * rg + 4 * g;
-            *reinterpret_cast<bf16x4 *>(dKb + d) =
-                pack4(dk[db][4 * rg] * scale, dk[db][4 * rg + 1] * scale,
-                      dk[db][4 * rg + 2] * scale, dk[db][4 * rg + 3] * scale);
-            *reinterpret_cast<bf16x4 *>(dVb + d) =
-                pack4(dv[db][4 * rg], dv[db][4 * rg + 1], dv[db][4 * rg + 2], dv[db][4 * rg + 3]);
+    // One query tile in LDS stage BUF; the next tile (of this item or the
+    // next one) goes to the other stage.  Returns false after the last item.
+    auto step = [&](auto bufc) __attribute__((always_inline)) -> bool {
+        constexpr int BUF = decltype(bufc)::value;
+        uint16_t *other = lds + (1 - BUF) * T::STAGE;
+        const bool last = t == it.t_end;
+        bool more = false;
+        if (!last) {
+            kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, it, t + 1, L, rs, wave, lane);
+        } else if constexpr (PERSIST) {
+            const int nbid = kv_item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
+            more = nbid >= 0;
+            if (more) {
+                nit = kv_item<D, T>(nbid, nkb, B, L, H, causal, cu, n_docs);
+                kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, nit, nit.t_begin, L, rs, wave,
+                               lane);
+            }
         }
+        compute(t, bufc);
+        if (more)  // K and V of the next item (registers free after the tile)
+            load_kv(nit);
+        wait_vmem();
+        __syncthreads();
+        if (!last) {
+            ++t;
+            return true;
+        }
+        store();
+        if (!PERSIST || !more)
+            return false;
+        ++k_item;
+        it = nit;
+        setup(it);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            dk[db] = f32x16{};
+            dv[db] = f32x16{};
+        }
+        t = it.t_begin;
+        return true;
+    };
+    for (;;) {
+        if (!step(IC<0>{}))
+            break;
+        if (!step(IC<1>{}))
+            break;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -483,7 +521,8 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const uint16_t *__restrict__, const uint16_t *__restrict__, const float *__restrict__,   \
         float *__restrict__, float *__restrict__, uint16_t *__restrict__, int, int, int, int,     \
         const int32_t *__restrict__, int, float, float, int, RopeEpi, int
-template __global__ void dkdv1_kernel<64>(DD_KV_ARGS);   // D = 64: single-role waves
+template __global__ void dkdv1_kernel<64, false>(DD_KV_ARGS);  // D = 64: single-role waves
+template __global__ void dkdv1_kernel<64, true>(DD_KV_ARGS);
 template __global__ void dq_kernel<64>(DD_Q_ARGS);
 template __global__ void dq_kernel<128>(DD_Q_ARGS);
 #undef DD_KV_ARGS
@@ -522,11 +561,20 @@ static int launch_bwd_d(const BwdArgs &a)
     {
         ProfScope prof(K_DKDV, st);
         if constexpr (D == 64) {
-            const int nkb = (a.L + KvTile1<D>::BN - 1) / KvTile1<D>::BN;
-            e = launch_kernel(dkdv1_kernel<D>, dim3(static_cast<unsigned>(nkb * a.B * a.H)),
-                              dim3(64 * KvTile1<D>::NW), st, a.Q, a.K, a.V, a.dO, lse2, delta,
-                              a.dK, a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs,
-                              s.scale_log2, s.scale, nkb, s.rt, s.rope);
+            using T = KvTile1<D>;
+            const int nkb = (a.L + T::BN - 1) / T::BN;
+            const long long n_items = static_cast<long long>(nkb) * a.B * a.H;
+            const long long all = (n_items + kXcds - 1) / kXcds * kXcds;
+            // Persistent for short spans: two workgroups per CU (registers
+            // admit two), a multiple of the XCD count.
+            const long long cus = doc_span_tokens(a) <= kPersistMaxSpan ? device_cu_count() : 0;
+            const bool persist = cus >= kXcds && 2 * cus < all;
+            auto kern = persist ? dkdv1_kernel<D, true> : dkdv1_kernel<D, false>;
+            const long long grid = persist ? 2 * (cus / kXcds) * kXcds : all;
+            e = launch_kernel(kern, dim3(static_cast<unsigned>(grid)), dim3(64 * T::NW), st, a.Q,
+                              a.K, a.V, a.dO, lse2, delta, a.dK, a.dV, a.B, a.L, a.H,
+                              a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale, nkb, s.rt,
+                              s.rope);
         } else {
             e = launch_dkdv_paired(a, s);
         }

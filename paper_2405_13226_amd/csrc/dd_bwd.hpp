@@ -6,6 +6,7 @@
 #include "dd_device.hpp"
 #include "dd_internal.h"
 #include "dd_rope.hpp"
+#include "dd_tile.hpp"
 
 namespace dd {
 
@@ -22,5 +23,89 @@ struct BwdScalars {
 // dK and dV for D = 128 with the paired-wave kernel (dd_dkdv.hip); returns the
 // runtime's launch status.
 hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s);
+
+// Compute units of the current device, cached per device id (0 on error).
+int device_cu_count();
+
+// Below this many tokens per document span (the row, or the mean document
+// length under document masking) a key block visits few query tiles, and the
+// persistent dK/dV forms, which hide each item's set-up behind the previous
+// item, are faster; above it the items are long and one item per workgroup
+// (hardware dispatch) is.
+constexpr long long kPersistMaxSpan = 1024;
+
+inline long long doc_span_tokens(const BwdArgs &a)
+{
+    if (!a.cu || a.n_docs < 1)
+        return a.L;
+    const long long mean = static_cast<long long>(a.B) * a.L / a.n_docs;
+    return mean < a.L ? mean : a.L;
+}
+
+// ---------------------------------------------------------------------------
+// Work items of the persistent dK/dV kernels
+// ---------------------------------------------------------------------------
+
+// Work item k of workgroup w among G (G a multiple of 8): the block id that
+// block_slice maps to a (slice, key block), or -1 past the last item.  Each
+// XCD's workgroups (w % 8 = x) take the XCD's block sequence n = 0, 1, ...
+// (block id 8n + x) in rounds of 2C (C = G / 8 workgroups per XCD), in
+// zig-zag order: workgroup c takes positions c and 2C-1-c of every round.
+// Under the causal mask a slice's key blocks cost linearly less work in
+// block order, so each workgroup's pair of a round sums to the same cost.
+__device__ __forceinline__ int kv_item_bid(int k, int w, int G, int n_items)
+{
+    const int x = w % kXcds, c = w / kXcds, C = G / kXcds;
+    const int n = 2 * C * (k >> 1) + ((k & 1) ? 2 * C - 1 - c : c);
+    const int bid = n * kXcds + x;
+    return bid < n_items ? bid : -1;
+}
+
+// A work item: one key block of one (b, h) slice and the query tiles its
+// keys are visible to.
+struct KvItem {
+    int b, bh, kvb, t_begin, t_end;
+    long long base;  // element offset of (b, row 0, h, 0)
+};
+
+// Tile shape T: T::BN keys per item, T::BM queries per tile.
+template <int D, class T>
+__device__ __forceinline__ KvItem kv_item(int bid, int nkb, int B, int L, int H, bool causal,
+                                          const int32_t *__restrict__ cu, int n_docs)
+{
+    KvItem it;
+    block_slice(bid, nkb, B * H, it.bh, it.kvb);
+    it.b = it.bh / H;
+    it.base = (static_cast<long long>(it.b) * L * H + it.bh % H) * D;
+    const int kf0 = it.kvb * T::BN, kl = min(kf0 + T::BN - 1, L - 1);
+    int wlo, whi, tmp;
+    key_queries(it.b, L, kf0, causal, cu, n_docs, wlo, tmp);
+    key_queries(it.b, L, kl, causal, cu, n_docs, tmp, whi);
+    it.t_begin = wlo / T::BM;
+    it.t_end = whi / T::BM;
+    return it;
+}
+
+// Direct-to-LDS loads of query tile t of item x into `stage`: the Q and dO
+// tiles (T::TILE elements each), then lse2 and delta of its rows (waves 0
+// and 1).
+template <int D, class T>
+__device__ __forceinline__ void kv_issue(const DmaPlan<D, T::BM, T::NW> &plan, uint16_t *stage,
+                                         const uint16_t *__restrict__ Q,
+                                         const uint16_t *__restrict__ dO,
+                                         const float *__restrict__ lse2g,
+                                         const float *__restrict__ deltag, const KvItem &x, int t,
+                                         int L, long long rs, int wave, int lane)
+{
+    const int i0 = t * T::BM;
+    plan.issue(stage, Q + x.base, rs, i0, L, wave, lane);
+    plan.issue(stage + T::TILE, dO + x.base, rs, i0, L, wave, lane);
+    float *fs = reinterpret_cast<float *>(stage + 2 * T::TILE);
+    if (wave == 0)
+        dma_row_f32(fs, lse2g + static_cast<long long>(x.bh) * L, i0, L, lane);
+    else if (wave == 1)
+        dma_row_f32(fs + T::BM, deltag + static_cast<long long>(x.bh) * L, i0, L, lane);
+}
+
 
 }  // namespace dd

@@ -32,67 +32,6 @@ constexpr int kSchedMfma = 0x008;
 constexpr int kSchedDsRead = 0x100;
 constexpr int kAhead = 4;
 
-// Work item k of workgroup w among G (G a multiple of 8): the block id that
-// block_slice maps to a (slice, key block), or -1 past the last item.  Each
-// XCD's workgroups (w % 8 = x) take the XCD's block sequence n = 0, 1, ...
-// (block id 8n + x) in rounds of 2C (C = G / 8 workgroups per XCD), in
-// zig-zag order: workgroup c takes positions c and 2C-1-c of every round.
-// Under the causal mask a slice's key blocks cost linearly less work in
-// block order, so each workgroup's pair of a round sums to the same cost.
-__device__ __forceinline__ int kv_item_bid(int k, int w, int G, int n_items)
-{
-    const int x = w % kXcds, c = w / kXcds, C = G / kXcds;
-    const int n = 2 * C * (k >> 1) + ((k & 1) ? 2 * C - 1 - c : c);
-    const int bid = n * kXcds + x;
-    return bid < n_items ? bid : -1;
-}
-
-// A work item: one key block of one (b, h) slice and the query tiles its
-// keys are visible to.
-struct KvItem {
-    int b, bh, kvb, t_begin, t_end;
-    long long base;  // element offset of (b, row 0, h, 0)
-};
-
-template <int D>
-__device__ __forceinline__ KvItem kv_item(int bid, int nkb, int B, int L, int H, bool causal,
-                                          const int32_t *__restrict__ cu, int n_docs)
-{
-    using T = KvTile<D>;
-    KvItem it;
-    block_slice(bid, nkb, B * H, it.bh, it.kvb);
-    it.b = it.bh / H;
-    it.base = (static_cast<long long>(it.b) * L * H + it.bh % H) * D;
-    const int kf0 = it.kvb * T::BN, kl = min(kf0 + T::BN - 1, L - 1);
-    int wlo, whi, tmp;
-    key_queries(it.b, L, kf0, causal, cu, n_docs, wlo, tmp);
-    key_queries(it.b, L, kl, causal, cu, n_docs, tmp, whi);
-    it.t_begin = wlo / T::BM;
-    it.t_end = whi / T::BM;
-    return it;
-}
-
-// Direct-to-LDS loads of query tile t of item x into `stage`: the Q and dO
-// tiles, then lse2 and delta of its rows (waves 0 and 1).
-template <int D>
-__device__ __forceinline__ void kv_issue(const DmaPlan<D, KvTile<D>::BM, KvTile<D>::NW> &plan,
-                                         uint16_t *stage, const uint16_t *__restrict__ Q,
-                                         const uint16_t *__restrict__ dO,
-                                         const float *__restrict__ lse2g,
-                                         const float *__restrict__ deltag, const KvItem &x, int t,
-                                         int L, long long rs, int wave, int lane)
-{
-    using T = KvTile<D>;
-    const int i0 = t * T::BM;
-    plan.issue(stage, Q + x.base, rs, i0, L, wave, lane);
-    plan.issue(stage + T::TILE, dO + x.base, rs, i0, L, wave, lane);
-    float *fs = reinterpret_cast<float *>(stage + 2 * T::TILE);
-    if (wave == 0)
-        dma_row_f32(fs, lse2g + static_cast<long long>(x.bh) * L, i0, L, lane);
-    else if (wave == 1)
-        dma_row_f32(fs + T::BM, deltag + static_cast<long long>(x.bh) * L, i0, L, lane);
-}
-
 // Key-resident dK/dV.  The 32 keys of a group are shared by two waves on the
 // same SIMD (wave w and w + 4):
 //   role A (waves 0-3): K in registers; S = Q K^T, P = exp2(S*c - lse2)
@@ -138,7 +77,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     int bid = kv_item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
     if (bid < 0)
         return;
-    KvItem it = kv_item<D>(bid, nkb, B, L, H, causal, cu, n_docs), nit = it;
+    KvItem it = kv_item<D, T>(bid, nkb, B, L, H, causal, cu, n_docs), nit = it;
 
     // Per-lane state of the current item.
     int my_k, qlo_k, qhi_k, lo_w, hi_w, lo_all, hi_all;
@@ -376,7 +315,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     for (int db = 0; db < DB; ++db)
         acc[db] = f32x16{};
     int t = it.t_begin;
-    kv_issue<D>(plan, lds, Q, dO, lse2g, deltag, it, t, L, rs, wave, lane);
+    kv_issue<D, T>(plan, lds, Q, dO, lse2g, deltag, it, t, L, rs, wave, lane);
     wait_vmem();
     __syncthreads();
 
@@ -388,13 +327,13 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const bool last = t == it.t_end;
         bool more = false;
         if (!last) {
-            kv_issue<D>(plan, other, Q, dO, lse2g, deltag, it, t + 1, L, rs, wave, lane);
+            kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, it, t + 1, L, rs, wave, lane);
         } else if constexpr (PERSIST) {
             const int nbid = kv_item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
             more = nbid >= 0;
             if (more) {
-                nit = kv_item<D>(nbid, nkb, B, L, H, causal, cu, n_docs);
-                kv_issue<D>(plan, other, Q, dO, lse2g, deltag, nit, nit.t_begin, L, rs, wave,
+                nit = kv_item<D, T>(nbid, nkb, B, L, H, causal, cu, n_docs);
+                kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, nit, nit.t_begin, L, rs, wave,
                                  lane);
             }
         }
@@ -434,8 +373,7 @@ template __global__ void dkdv_kernel<128, false>(DD_KV_ARGS);
 template __global__ void dkdv_kernel<128, true>(DD_KV_ARGS);
 #undef DD_KV_ARGS
 
-// Compute units of the current device, cached per device id.
-static int device_cu_count()
+int device_cu_count()
 {
     constexpr int kMaxDevices = 64;
     static std::atomic<int> cache[kMaxDevices];
@@ -455,22 +393,13 @@ static int device_cu_count()
     return n;
 }
 
-// Below this many tokens per document span (the row, or the mean document
-// length under document masking) a key block visits few query tiles, and
-// the persistent form, which hides each item's set-up behind the previous
-// item, is faster; above it the items are long and one item per workgroup
-// (hardware dispatch) is.
-constexpr long long kPersistMaxSpan = 1024;
-
 hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s)
 {
     using T = KvTile<128>;
     const int nkb = (a.L + T::BN - 1) / T::BN;
     const long long n_items = static_cast<long long>(nkb) * a.B * a.H;
     const long long all = (n_items + kXcds - 1) / kXcds * kXcds;
-    const long long span = a.cu ? std::min<long long>(a.L, static_cast<long long>(a.B) * a.L /
-                                                               std::max(a.n_docs, 1))
-                                : a.L;
+    const long long span = doc_span_tokens(a);
     hipStream_t st = static_cast<hipStream_t>(a.stream);
     if (span > kPersistMaxSpan)
         return launch_kernel(dkdv_kernel<128, false>, dim3(static_cast<unsigned>(all)),
