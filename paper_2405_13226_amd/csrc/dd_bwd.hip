@@ -565,12 +565,14 @@ static int launch_bwd_d(const BwdArgs &a)
             const int nkb = (a.L + T::BN - 1) / T::BN;
             const long long n_items = static_cast<long long>(nkb) * a.B * a.H;
             const long long all = (n_items + kXcds - 1) / kXcds * kXcds;
-            // Persistent for short spans: two workgroups per CU (registers
-            // admit two), a multiple of the XCD count.
-            const long long cus = doc_span_tokens(a) <= kPersistMaxSpan ? device_cu_count() : 0;
-            const bool persist = cus >= kXcds && 2 * cus < all;
+            // Persistent for short spans, as many workgroups as are resident
+            // at once (two per CU).
+            const long long pgrid = doc_span_tokens(a) <= kPersistMaxSpan
+                                        ? persistent_grid<dkdv1_kernel<D, true>>(64 * T::NW)
+                                        : 0;
+            const bool persist = pgrid > 0 && pgrid < all;
             auto kern = persist ? dkdv1_kernel<D, true> : dkdv1_kernel<D, false>;
-            const long long grid = persist ? 2 * (cus / kXcds) * kXcds : all;
+            const long long grid = persist ? pgrid : all;
             e = launch_kernel(kern, dim3(static_cast<unsigned>(grid)), dim3(64 * T::NW), st, a.Q,
                               a.K, a.V, a.dO, lse2, delta, a.dK, a.dV, a.B, a.L, a.H,
                               a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale, nkb, s.rt,

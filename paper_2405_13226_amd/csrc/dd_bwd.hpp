@@ -8,6 +8,8 @@
 #include "dd_rope.hpp"
 #include "dd_tile.hpp"
 
+#include <atomic>
+
 namespace dd {
 
 // Per-call values every backward kernel takes, derived once by the launcher.
@@ -26,6 +28,25 @@ hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s);
 
 // Compute units of the current device, cached per device id (0 on error).
 int device_cu_count();
+
+// Workgroups of a persistent launch of kernel KERN with `block` threads: as
+// many as are resident at once (the runtime's occupancy for the kernel, per
+// CU, times the CU count), rounded down to a multiple of the XCD count; 0 on
+// error.  The per-CU figure is cached per kernel.
+template <auto KERN>
+long long persistent_grid(int block)
+{
+    static std::atomic<int> per_cu{-1};
+    int n = per_cu.load(std::memory_order_relaxed);
+    if (n < 0) {
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &n, reinterpret_cast<const void *>(KERN), block, 0) != hipSuccess)
+            return 0;
+        per_cu.store(n, std::memory_order_relaxed);
+    }
+    const long long wgs = static_cast<long long>(n) * device_cu_count();
+    return wgs / kXcds * kXcds;
+}
 
 // Below this many tokens per document span (the row, or the mean document
 // length under document masking) a key block visits few query tiles, and the

@@ -406,12 +406,11 @@ hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s)
                              dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.delta, a.dK,
                              a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2,
                              s.scale, nkb, s.rt, s.rope);
-    // Persistent: at most one workgroup per CU (registers and LDS admit one),
-    // a multiple of the XCD count.
-    const long long cus = device_cu_count();
-    if (cus < kXcds)
+    // Persistent: as many workgroups as are resident at once (one per CU).
+    const long long pgrid = persistent_grid<dkdv_kernel<128, true>>(64 * T::NW);
+    if (pgrid <= 0)
         return hipErrorInvalidDevice;
-    const long long grid = std::min((cus / kXcds) * kXcds, all);
+    const long long grid = std::min(pgrid, all);
     return launch_kernel(dkdv_kernel<128, true>, dim3(static_cast<unsigned>(grid)),
                          dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.delta, a.dK, a.dV,
                          a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale,
