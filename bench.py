@@ -236,9 +236,9 @@ def workload(name, seed, buckets=None):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the attention "
-              "path has no cross-GPU exchange and this build measures a single MI355X.",
-              file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): every (b, h) slice "
+              "of the attention path is independent, so there is no cross-GPU exchange to "
+              "measure; the figure is one MI355X's throughput.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
