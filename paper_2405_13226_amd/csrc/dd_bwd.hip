@@ -41,7 +41,7 @@ namespace dd {
 // for several waves per SIMD.
 //
 // PERSIST = false: one work item (key block) per workgroup.  PERSIST = true:
-// a workgroup walks its work items (kv_item_bid) back to back; during an
+// a workgroup walks its work items (item_bid) back to back; during an
 // item's last query tile it loads the next item's first Q/dO tile into the
 // free LDS stage, and after that tile the next item's K and V rows (holding
 // them during the tile as well would spill at D = 64).
@@ -76,7 +76,7 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const int G = static_cast<int>(gridDim.x);
 
     int k_item = 0;
-    const int bid = kv_item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
+    const int bid = item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
     if (bid < 0)
         return;
     KvItem it = kv_item<D, T>(bid, nkb, B, L, H, causal, cu, n_docs), nit = it;
@@ -243,7 +243,7 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         if (!last) {
             kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, it, t + 1, L, rs, wave, lane);
         } else if constexpr (PERSIST) {
-            const int nbid = kv_item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
+            const int nbid = item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
             more = nbid >= 0;
             if (more) {
                 nit = kv_item<D, T>(nbid, nkb, B, L, H, causal, cu, n_docs);

@@ -8,7 +8,6 @@
 #include "dd_rope.hpp"
 #include "dd_tile.hpp"
 
-#include <atomic>
 
 namespace dd {
 
@@ -25,28 +24,6 @@ struct BwdScalars {
 // dK and dV for D = 128 with the paired-wave kernel (dd_dkdv.hip); returns the
 // runtime's launch status.
 hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s);
-
-// Compute units of the current device, cached per device id (0 on error).
-int device_cu_count();
-
-// Workgroups of a persistent launch of kernel KERN with `block` threads: as
-// many as are resident at once (the runtime's occupancy for the kernel, per
-// CU, times the CU count), rounded down to a multiple of the XCD count; 0 on
-// error.  The per-CU figure is cached per kernel.
-template <auto KERN>
-long long persistent_grid(int block)
-{
-    static std::atomic<int> per_cu{-1};
-    int n = per_cu.load(std::memory_order_relaxed);
-    if (n < 0) {
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &n, reinterpret_cast<const void *>(KERN), block, 0) != hipSuccess)
-            return 0;
-        per_cu.store(n, std::memory_order_relaxed);
-    }
-    const long long wgs = static_cast<long long>(n) * device_cu_count();
-    return wgs / kXcds * kXcds;
-}
 
 // Below this many tokens per document span (the row, or the mean document
 // length under document masking) a key block visits few query tiles, and the
@@ -66,21 +43,6 @@ inline long long doc_span_tokens(const BwdArgs &a)
 // ---------------------------------------------------------------------------
 // Work items of the persistent dK/dV kernels
 // ---------------------------------------------------------------------------
-
-// Work item k of workgroup w among G (G a multiple of 8): the block id that
-// block_slice maps to a (slice, key block), or -1 past the last item.  Each
-// XCD's workgroups (w % 8 = x) take the XCD's block sequence n = 0, 1, ...
-// (block id 8n + x) in rounds of 2C (C = G / 8 workgroups per XCD), in
-// zig-zag order: workgroup c takes positions c and 2C-1-c of every round.
-// Under the causal mask a slice's key blocks cost linearly less work in
-// block order, so each workgroup's pair of a round sums to the same cost.
-__device__ __forceinline__ int kv_item_bid(int k, int w, int G, int n_items)
-{
-    const int x = w % kXcds, c = w / kXcds, C = G / kXcds;
-    const int n = 2 * C * (k >> 1) + ((k & 1) ? 2 * C - 1 - c : c);
-    const int bid = n * kXcds + x;
-    return bid < n_items ? bid : -1;
-}
 
 // A work item: one key block of one (b, h) slice and the query tiles its
 // keys are visible to.

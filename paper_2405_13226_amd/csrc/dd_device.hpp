@@ -133,6 +133,21 @@ __device__ __forceinline__ void block_slice(int bid, int nblk, int BH, int &bh, 
     }
 }
 
+// Work item k of workgroup w among G (G a multiple of 8): the block id that
+// block_slice maps to a (slice, block), or -1 past the last item.  Each
+// XCD's workgroups (w % 8 = x) take the XCD's block sequence n = 0, 1, ...
+// (block id 8n + x) in rounds of 2C (C = G / 8 workgroups per XCD), in
+// zig-zag order: workgroup c takes positions c and 2C-1-c of every round.
+// Under the causal mask a slice's blocks cost linearly less (or more) work
+// in block order, so each workgroup's pair of a round sums to the same cost.
+__device__ __forceinline__ int item_bid(int k, int w, int G, int n_items)
+{
+    const int x = w % kXcds, c = w / kXcds, C = G / kXcds;
+    const int n = 2 * C * (k >> 1) + ((k & 1) ? 2 * C - 1 - c : c);
+    const int bid = n * kXcds + x;
+    return bid < n_items ? bid : -1;
+}
+
 // Wave-wide min / max of an int.
 __device__ __forceinline__ int wave_min(int v)
 {

@@ -43,7 +43,7 @@ constexpr int kAhead = 4;
 // wave's softmax arithmetic overlaps the other's matrix products.
 //
 // PERSIST = false: one work item per workgroup (grid = all items).
-// PERSIST = true: a workgroup walks its work items (kv_item_bid) back to
+// PERSIST = true: a workgroup walks its work items (item_bid) back to
 // back.  During the last query tile of an item it already loads the next
 // item's first Q/dO tile into the free LDS stage, and after that tile's
 // mid-tile barrier (when K or V in registers is no longer needed) the next
@@ -74,7 +74,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const int G = static_cast<int>(gridDim.x);
 
     int k_item = 0;
-    int bid = kv_item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
+    int bid = item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
     if (bid < 0)
         return;
     KvItem it = kv_item<D, T>(bid, nkb, B, L, H, causal, cu, n_docs), nit = it;
@@ -329,7 +329,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         if (!last) {
             kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, it, t + 1, L, rs, wave, lane);
         } else if constexpr (PERSIST) {
-            const int nbid = kv_item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
+            const int nbid = item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
             more = nbid >= 0;
             if (more) {
                 nit = kv_item<D, T>(nbid, nkb, B, L, H, causal, cu, n_docs);

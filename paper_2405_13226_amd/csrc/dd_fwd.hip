@@ -23,6 +23,8 @@
 #include "dd_prof.hpp"
 #include "dd_attn.h"
 
+#include <algorithm>
+
 namespace dd {
 
 template <int D>
@@ -39,7 +41,42 @@ struct FwdTile {
 // unchanged.
 constexpr float kRescaleSlack = 8.0f;
 
+// Spans (tokens) up to which the forward runs persistently.
+constexpr long long kFwdPersistMaxSpan = 2048;
+
+// A query-block work item of the forward: one block of FwdTile::BM queries of
+// one (b, h) slice and the key tiles those queries see.
+struct FwdItem {
+    int b, bh, qb, t_begin, t_end;
+    long long base;  // element offset of (b, row 0, h, 0)
+};
+
 template <int D>
+__device__ __forceinline__ FwdItem fwd_item(int bid, int nqb, int B, int L, int H, bool causal,
+                                            const int32_t *__restrict__ cu, int n_docs)
+{
+    using T = FwdTile<D>;
+    FwdItem it;
+    int jb;
+    block_slice(bid, nqb, B * H, it.bh, jb);
+    it.qb = nqb - 1 - jb;  // heaviest query blocks (the last) first
+    it.b = it.bh / H;
+    it.base = (static_cast<long long>(it.b) * L * H + it.bh % H) * D;
+    // Key range: union over the block's queries (monotone in the query).
+    const int qf = it.qb * T::BM, ql = min(qf + T::BM - 1, L - 1);
+    int wlo, whi, tmp;
+    query_keys(it.b, L, qf, causal, cu, n_docs, wlo, tmp);
+    query_keys(it.b, L, ql, causal, cu, n_docs, tmp, whi);
+    it.t_begin = wlo / T::BN;
+    it.t_end = whi / T::BN;
+    return it;
+}
+
+// PERSIST = false: one query block per workgroup.  PERSIST = true (short
+// spans): a workgroup walks its query blocks in the order of item_bid; during
+// a block's last key tile it DMAs the next block's first K/V tile into the
+// free stage, and after that tile loads the next block's Q rows.
+template <int D, bool PERSIST>
 __global__ void __launch_bounds__(256, 2)
 fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
            const uint16_t *__restrict__ V, uint16_t *__restrict__ O, float *__restrict__ LSE,
@@ -54,48 +91,46 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
-
-    // Slices grouped per XCD, heaviest query blocks (the last) first.
-    const int BH = B * H;
-    int bh, jb;
-    block_slice(blockIdx.x, nqb, BH, bh, jb);
-    const int qb = nqb - 1 - jb;
-    const int b = bh / H, h = bh % H;
-
     const long long rs = static_cast<long long>(H) * D;  // token stride
-    const long long base = (static_cast<long long>(b) * L * H + h) * D;
-    const uint16_t *Qb = Q + base, *Kb = K + base, *Vb = V + base;
+    const int n_items = nqb * B * H;
+    const int G = static_cast<int>(gridDim.x);
 
-    // This lane's query and its allowed keys.
-    const int q0w = qb * T::BM + wave * 32;
-    const int my_q = q0w + l32;
-    const bool q_ok = my_q < L;
-    int lo_q = 1, hi_q = 0;  // empty for padding rows
-    if (q_ok)
-        query_keys(b, L, my_q, causal, cu, n_docs, lo_q, hi_q);
-    const bool wave_on = q0w < L;
-    const int lo_w = wave_min(q_ok ? lo_q : 0x7fffffff);
-    const int hi_w = wave_max(q_ok ? hi_q : -1);
-    const int lo_all = wave_max(q_ok ? lo_q : -1);
-    const int hi_all = wave_min(q_ok ? hi_q : 0x7fffffff);
-    const bool wave_full_rows = (q0w + 31) < L;
+    int k_item = 0;
+    const int bid = item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
+    if (bid < 0)
+        return;
+    FwdItem it = fwd_item<D>(bid, nqb, B, L, H, causal, cu, n_docs), nit = it;
 
-    // Workgroup key range: union over its queries (monotone in the query).
-    const int qf = qb * T::BM, ql = min(qb * T::BM + T::BM - 1, L - 1);
-    int wlo, whi, tmp;
-    query_keys(b, L, qf, causal, cu, n_docs, wlo, tmp);
-    query_keys(b, L, ql, causal, cu, n_docs, tmp, whi);
-    const int t_begin = wlo / T::BN, t_end = whi / T::BN;
-
-    // Q fragments (B operand: column = query, k-slots = 8 head dims).
-    bf16x8 qf8[KK];
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-        u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    // This lane's query and its allowed keys (per item).
+    int my_q, lo_q, hi_q, lo_w, hi_w, lo_all, hi_all;
+    bool q_ok, wave_on, wave_full_rows;
+    auto setup = [&](const FwdItem &x) __attribute__((always_inline)) {
+        const int q0w = x.qb * T::BM + wave * 32;
+        my_q = q0w + l32;
+        q_ok = my_q < L;
+        lo_q = 1;  // empty for padding rows
+        hi_q = 0;
         if (q_ok)
-            v = *reinterpret_cast<const u32x4 *>(Qb + my_q * rs + kk * 16 + g * 8);
-        qf8[kk] = as_bf16x8(v);
-    }
+            query_keys(x.b, L, my_q, causal, cu, n_docs, lo_q, hi_q);
+        wave_on = q0w < L;
+        lo_w = wave_min(q_ok ? lo_q : 0x7fffffff);
+        hi_w = wave_max(q_ok ? hi_q : -1);
+        lo_all = wave_max(q_ok ? lo_q : -1);
+        hi_all = wave_min(q_ok ? hi_q : 0x7fffffff);
+        wave_full_rows = (q0w + 31) < L;
+    };
+
+    // Q fragments (B operand: column = query, k-slots = 8 head dims).  A
+    // query past L reads row L-1 instead (its scores are masked out and
+    // nothing of it is stored).
+    bf16x8 qf8[KK];
+    auto load_q = [&](const FwdItem &x) __attribute__((always_inline)) {
+        const int q = min(x.qb * T::BM + wave * 32 + l32, L - 1);
+        const uint16_t *src = Q + x.base + q * rs + g * 8;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+            qf8[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(src + kk * 16));
+    };
 
     // Per-lane LDS offsets (elements, relative to a tile).  K row reads: row
     // l32 of a 32-key block, chunk 2*kk + g.  V transposed reads: rows
@@ -114,16 +149,13 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     }
 
     f32x16 acc[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-        acc[db] = f32x16{};
     float m_i = -INFINITY, l_i = 0.f;
 
     DmaPlan<D, T::BN, 4> plan;
     plan.init(rs, wave, lane);
-    auto issue = [&](int t, uint16_t *stage) {
-        plan.issue(stage, Kb, rs, t * T::BN, L, wave, lane);
-        plan.issue(stage + T::TILE, Vb, rs, t * T::BN, L, wave, lane);
+    auto issue = [&](const FwdItem &x, int t, uint16_t *stage) __attribute__((always_inline)) {
+        plan.issue(stage, K + x.base, rs, t * T::BN, L, wave, lane);
+        plan.issue(stage + T::TILE, V + x.base, rs, t * T::BN, L, wave, lane);
     };
 
     // One tile; MASKED selects the boundary-tile variant at compile time.
@@ -218,67 +250,116 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             body(j0, bufc, IC<1>{});
     };
 
-    issue(t_begin, lds);
+    // O = acc / l and the LSE of the current item.
+    auto store = [&]() __attribute__((always_inline)) {
+        if (!q_ok)
+            return;
+        const float l_tot = l_i + __shfl_xor(l_i, 32);
+        const float inv = 1.0f / l_tot;
+        uint16_t *Ob = O + it.base + my_q * rs;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+                const int d = db * 32 + 8 * rg + 4 * g;
+                const bf16x4 v = pack4(acc[db][4 * rg] * inv, acc[db][4 * rg + 1] * inv,
+                                       acc[db][4 * rg + 2] * inv, acc[db][4 * rg + 3] * inv);
+                *reinterpret_cast<bf16x4 *>(Ob + d) = v;
+            }
+        if (g == 0)
+            LSE[(static_cast<long long>(it.b) * L + my_q) * H + it.bh % H] =
+                (m_i + log2f(l_tot)) * kLn2;
+    };
+    auto reset = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+            acc[db] = f32x16{};
+        m_i = -INFINITY;
+        l_i = 0.f;
+    };
+
+    setup(it);
+    load_q(it);
+    reset();
+    int t = it.t_begin;
+    issue(it, t, lds);
     wait_vmem();
     __syncthreads();
-    for (int t = t_begin;;) {
-        if (t < t_end)
-            issue(t + 1, lds + T::STAGE);
-        compute(t, IC<0>{});
-        wait_vmem();
-        __syncthreads();
-        if (t == t_end)
-            break;
-        ++t;
-        if (t < t_end)
-            issue(t + 1, lds);
-        compute(t, IC<1>{});
-        wait_vmem();
-        __syncthreads();
-        if (t == t_end)
-            break;
-        ++t;
-    }
 
-    if (!q_ok)
-        return;
-    const float l_tot = l_i + __shfl_xor(l_i, 32);
-    const float inv = 1.0f / l_tot;
-    uint16_t *Ob = O + base + my_q * rs;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-            const int d = db * 32 + 8 * rg + 4 * g;
-            const bf16x4 v = pack4(acc[db][4 * rg] * inv, acc[db][4 * rg + 1] * inv,
-                                   acc[db][4 * rg + 2] * inv, acc[db][4 * rg + 3] * inv);
-            *reinterpret_cast<bf16x4 *>(Ob + d) = v;
+    // One key tile in LDS stage BUF; the next tile (of this item or the next
+    // one) goes to the other stage.  Returns false after the last item.
+    auto step = [&](auto bufc) __attribute__((always_inline)) -> bool {
+        constexpr int BUF = decltype(bufc)::value;
+        uint16_t *other = lds + (1 - BUF) * T::STAGE;
+        const bool last = t == it.t_end;
+        bool more = false;
+        if (!last) {
+            issue(it, t + 1, other);
+        } else if constexpr (PERSIST) {
+            const int nbid = item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
+            more = nbid >= 0;
+            if (more) {
+                nit = fwd_item<D>(nbid, nqb, B, L, H, causal, cu, n_docs);
+                issue(nit, nit.t_begin, other);
+            }
         }
-    if (g == 0)
-        LSE[(static_cast<long long>(b) * L + my_q) * H + h] = (m_i + log2f(l_tot)) * kLn2;
+        compute(t, bufc);
+        if (more)  // Q of the next item (registers free after the tile)
+            load_q(nit);
+        wait_vmem();
+        __syncthreads();
+        if (!last) {
+            ++t;
+            return true;
+        }
+        store();
+        if (!PERSIST || !more)
+            return false;
+        ++k_item;
+        it = nit;
+        setup(it);
+        reset();
+        t = it.t_begin;
+        return true;
+    };
+    for (;;) {
+        if (!step(IC<0>{}))
+            break;
+        if (!step(IC<1>{}))
+            break;
+    }
 }
 
 // Explicit instantiations: the host-side launch stubs are emitted here
 // unconditionally (clang's host pass does not always emit them for templates
 // only referenced through a function pointer).
-template __global__ void fwd_kernel<64>(const uint16_t *__restrict__, const uint16_t *__restrict__,
-                                        const uint16_t *__restrict__, uint16_t *__restrict__,
-                                        float *__restrict__, int, int, int, int,
-                                        const int32_t *__restrict__, int, float, int);
-template __global__ void fwd_kernel<128>(const uint16_t *__restrict__, const uint16_t *__restrict__,
-                                         const uint16_t *__restrict__, uint16_t *__restrict__,
-                                         float *__restrict__, int, int, int, int,
-                                         const int32_t *__restrict__, int, float, int);
+#define DD_FWD_ARGS                                                                              \
+    const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,   \
+        uint16_t *__restrict__, float *__restrict__, int, int, int, int,                          \
+        const int32_t *__restrict__, int, float, int
+template __global__ void fwd_kernel<64, false>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<64, true>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<128, false>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<128, true>(DD_FWD_ARGS);
+#undef DD_FWD_ARGS
 
 template <int D>
 static int launch_fwd_d(const FwdArgs &a)
 {
     const int nqb = (a.L + FwdTile<D>::BM - 1) / FwdTile<D>::BM;
-    const long long blocks = static_cast<long long>(nqb) * a.B * a.H;
+    const long long all = (static_cast<long long>(nqb) * a.B * a.H + kXcds - 1) / kXcds * kXcds;
     const float scale_log2 = kLog2e / sqrtf(static_cast<float>(D));
+    // Persistent for short spans (the row, or the mean document length under
+    // document masking): as many workgroups as are resident at once.
+    const long long span =
+        a.cu && a.n_docs > 0 ? std::min<long long>(a.L, static_cast<long long>(a.B) * a.L / a.n_docs)
+                             : a.L;
+    const long long pgrid = span <= kFwdPersistMaxSpan ? persistent_grid<fwd_kernel<D, true>>(256) : 0;
+    const bool persist = pgrid > 0 && pgrid < all;
     ProfScope prof(K_FWD, static_cast<hipStream_t>(a.stream));
     const hipError_t e = launch_kernel(
-        fwd_kernel<D>, dim3(static_cast<unsigned>(blocks)), dim3(256),
+        persist ? fwd_kernel<D, true> : fwd_kernel<D, false>,
+        dim3(static_cast<unsigned>(persist ? pgrid : all)), dim3(256),
         static_cast<hipStream_t>(a.stream), a.Q, a.K, a.V, a.O, a.LSE, a.B, a.L, a.H,
         a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, nqb);
     return e == hipSuccess ? DD_OK : DD_ERR_HIP;

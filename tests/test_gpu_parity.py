@@ -39,29 +39,29 @@ def test_document_masked_chunks(cuda, D, causal):
     check_case(B, L, H, D, causal=causal, cu=cu, seed=D + causal)
 
 
-# Spans of <= 1024 tokens take the persistent dK/dV kernels, where a
-# workgroup walks several key blocks back to back: one workgroup per CU at
-# D = 128 (256), two at D = 64 (512).  B x 3 slices of L = 700 hold 6 key
-# blocks each: 432 at B = 24 (D = 128), 864 at B = 48 (D = 64), so the last
-# slices have blocks in a workgroup's second item; the last block of every
-# slice holds 60 keys (ragged).  With documents the span is their mean length.
-PERSIST_CASES = {128: (24, [(0, 0), (7, 1), (15, 0), (16, 2), (23, 2)]),
+# Short spans take the persistent forms of the forward and dK/dV kernels,
+# where a workgroup walks several blocks back to back.  Grids: forward 768
+# (D = 64) / 512 (D = 128) workgroups, dK/dV 512 / 256.  48 x 3 slices of
+# L = 700 hold 6 query blocks and 6 key blocks each (864 of each), so the last
+# slices fall in a workgroup's second (or later) item; the last block of every
+# slice holds 60 rows (ragged).  With documents the span is their mean length.
+PERSIST_CASES = {128: (48, [(0, 0), (15, 1), (31, 0), (40, 2), (47, 2)]),
                  64: (48, [(0, 0), (15, 1), (31, 0), (40, 2), (47, 2)])}
 
 
 @pytest.mark.parametrize("D", [64, 128])
-def test_persistent_dkdv_several_items_per_workgroup(cuda, D):
+def test_persistent_kernels_several_items_per_workgroup(cuda, D):
     B, bh = PERSIST_CASES[D]
-    check_case(B, 700, 3, D, causal=True, seed=11, bh=bh, tag=f"persistent dK/dV D={D}")
+    check_case(B, 700, 3, D, causal=True, seed=11, bh=bh, tag=f"persistent D={D}")
 
 
 @pytest.mark.parametrize("D", [64, 128])
-def test_persistent_dkdv_document_masked(cuda, D):
+def test_persistent_kernels_document_masked(cuda, D):
     (B, bh), L, H = PERSIST_CASES[D], 700, 3
     lens = synth.lognormal_doc_lengths(2, total_tokens=B * L, median=300, sigma=0.8)
     cu = dd.chunk_doclens(lens, B * L)
     check_case(B, L, H, D, causal=True, cu=cu, seed=12, bh=bh,
-               tag=f"persistent dK/dV D={D}, documents")
+               tag=f"persistent D={D}, documents")
 
 
 def test_single_token_documents(cuda):
