@@ -293,7 +293,43 @@ struct QTile {
     static constexpr int STAGE = 2 * TILE; // K then V
 };
 
+// Spans (tokens) up to which dQ runs persistently (D = 64).
+constexpr long long kDqPersistMaxSpan = 2048;
+
+// A query-block work item of the dQ kernel: one block of QTile::BM queries
+// of one (b, h) slice and the key tiles those queries see.
+struct QItem {
+    int b, bh, qb, t_begin, t_end;
+    long long base;  // element offset of (b, row 0, h, 0)
+};
+
 template <int D>
+__device__ __forceinline__ QItem q_item(int bid, int nqb, int B, int L, int H, bool causal,
+                                        const int32_t *__restrict__ cu, int n_docs)
+{
+    using T = QTile<D>;
+    QItem it;
+    int jb;
+    block_slice(bid, nqb, B * H, it.bh, jb);
+    it.qb = nqb - 1 - jb;  // the last query blocks see the most keys: first
+    it.b = it.bh / H;
+    it.base = (static_cast<long long>(it.b) * L * H + it.bh % H) * D;
+    const int qf0 = it.qb * T::BM, ql = min(qf0 + T::BM - 1, L - 1);
+    int wlo, whi, tmp;
+    query_keys(it.b, L, qf0, causal, cu, n_docs, wlo, tmp);
+    query_keys(it.b, L, ql, causal, cu, n_docs, tmp, whi);
+    it.t_begin = wlo / T::BN;
+    it.t_end = whi / T::BN;
+    return it;
+}
+
+// PERSIST = false: one query block per workgroup.  PERSIST = true (short
+// spans, D = 64 only; at D = 128 the item loop spills): a workgroup walks
+// its query blocks in the order of item_bid;
+// during a block's last key tile it DMAs the next block's first K/V tile
+// into the free stage, and right after that tile loads the next block's Q,
+// dO and O rows.
+template <int D, bool PERSIST>
 __global__ void __launch_bounds__(256, 2)
 dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
           const uint16_t *__restrict__ V, const uint16_t *__restrict__ O,
@@ -311,90 +347,92 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, l32 = lane & 31, g = lane >> 5;
-
-    const int BH = B * H;
-    int bh, jb;
-    block_slice(blockIdx.x, nqb, BH, bh, jb);
-    const int qb = nqb - 1 - jb;
-    const int b = bh / H, h = bh % H;
-
     const long long rs = static_cast<long long>(H) * D;
-    const long long base = (static_cast<long long>(b) * L * H + h) * D;
-    const uint16_t *Kb = K + base, *Vb = V + base;
+    const int n_items = nqb * B * H;
+    const int G = static_cast<int>(gridDim.x);
 
-    const int q0w = qb * T::BM + wave * 32;
-    const int my_q = q0w + l32;
-    const bool q_ok = my_q < L;
-    int lo_q = 1, hi_q = 0;
-    if (q_ok)
-        query_keys(b, L, my_q, causal, cu, n_docs, lo_q, hi_q);
-    const bool wave_on = q0w < L;
-    const int lo_w = wave_min(q_ok ? lo_q : 0x7fffffff);
-    const int hi_w = wave_max(q_ok ? hi_q : -1);
-    const int lo_all = wave_max(q_ok ? lo_q : -1);
-    const int hi_all = wave_min(q_ok ? hi_q : 0x7fffffff);
-    const bool wave_full_rows = (q0w + 31) < L;
+    int k_item = 0;
+    const int bid = item_bid(0, static_cast<int>(blockIdx.x), G, n_items);
+    if (bid < 0)
+        return;
+    QItem it = q_item<D>(bid, nqb, B, L, H, causal, cu, n_docs), nit = it;
 
-    const int qf0 = qb * T::BM, ql = min(qb * T::BM + T::BM - 1, L - 1);
-    int wlo, whi, tmp;
-    query_keys(b, L, qf0, causal, cu, n_docs, wlo, tmp);
-    query_keys(b, L, ql, causal, cu, n_docs, tmp, whi);
-    const int t_begin = wlo / T::BN, t_end = whi / T::BN;
+    // Per-lane state of the current item.
+    int my_q, lo_q, hi_q, lo_w, hi_w, lo_all, hi_all;
+    bool q_ok, wave_on, wave_full_rows;
+    auto setup = [&](const QItem &x) __attribute__((always_inline)) {
+        const int q0w = x.qb * T::BM + wave * 32;
+        my_q = q0w + l32;
+        q_ok = my_q < L;
+        lo_q = 1;
+        hi_q = 0;
+        if (q_ok)
+            query_keys(x.b, L, my_q, causal, cu, n_docs, lo_q, hi_q);
+        wave_on = q0w < L;
+        lo_w = wave_min(q_ok ? lo_q : 0x7fffffff);
+        hi_w = wave_max(q_ok ? hi_q : -1);
+        lo_all = wave_max(q_ok ? lo_q : -1);
+        hi_all = wave_min(q_ok ? hi_q : 0x7fffffff);
+        wave_full_rows = (q0w + 31) < L;
+    };
 
-    // Q and dO rows of this lane's query (k-slots 8g..8g+7 of each 16-wide
-    // step), and delta = rowsum(dO * O) from the same slots of O: a partial
-    // per lane, completed with the lane holding the other half of the row.
-    bf16x8 qf[KK], dof[KK];
-    float part = 0.f;
+    // Q, dO and O rows of this lane's query (k-slots 8g..8g+7 of each
+    // 16-wide step; load_rows), then delta = rowsum(dO * O): a partial per
+    // lane, completed with the lane holding the other half of the row; with
+    // the LSE in log2 units both are written, in [B*H][L] rows, for the dK/dV
+    // kernel that runs after this one (finish_rows).  A query past L reads
+    // row L-1 instead (its probabilities are masked to exactly 0 by a select
+    // and nothing of it is stored).
+    bf16x8 qf[KK], dof[KK], of[KK];
+    float neg_lse2 = 0.f, my_delta = 0.f;
+    auto load_rows = [&](const QItem &x) __attribute__((always_inline)) {
+        const int qrow = min(x.qb * T::BM + wave * 32 + l32, L - 1);
+        const long long at = x.base + qrow * rs + g * 8;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-        u32x4 qv = u32x4{0u, 0u, 0u, 0u}, dv = u32x4{0u, 0u, 0u, 0u}, ov = dv;
-        if (q_ok) {
-            const long long at = base + my_q * rs + kk * 16 + g * 8;
-            qv = *reinterpret_cast<const u32x4 *>(Q + at);
-            dv = *reinterpret_cast<const u32x4 *>(dO + at);
-            ov = *reinterpret_cast<const u32x4 *>(O + at);
+        for (int kk = 0; kk < KK; ++kk) {
+            qf[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(Q + at + kk * 16));
+            dof[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(dO + at + kk * 16));
+            of[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(O + at + kk * 16));
         }
-        qf[kk] = as_bf16x8(qv);
-        dof[kk] = as_bf16x8(dv);
-        const bf16x8 ob = as_bf16x8(ov);
+    };
+    auto finish_rows = [&](const QItem &x) __attribute__((always_inline)) {
+        const int q = x.qb * T::BM + wave * 32 + l32, qrow = min(q, L - 1);
+        float part = 0.f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-            part += static_cast<float>(ob[i]) * static_cast<float>(dof[kk][i]);
-    }
-    const float my_delta = part + __shfl_xor(part, 32);
-    const float lse2 = q_ok ? LSE[(static_cast<long long>(b) * L + my_q) * H + h] * kLog2e : 0.f;
-    const float neg_lse2 = -lse2;
-    // Both, in [B*H][L] rows, for the dK/dV kernel that runs after this one.
-    if (q_ok && g == 0) {
-        const long long wrow = static_cast<long long>(bh) * L;
-        deltag[wrow + my_q] = my_delta;
-        lse2g[wrow + my_q] = lse2;
-    }
+        for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                part += static_cast<float>(of[kk][i]) * static_cast<float>(dof[kk][i]);
+        my_delta = part + __shfl_xor(part, 32);
+        const float lse2 =
+            LSE[(static_cast<long long>(x.b) * L + qrow) * H + x.bh % H] * kLog2e;
+        neg_lse2 = -lse2;
+        if (q < L && g == 0) {
+            const long long wrow = static_cast<long long>(x.bh) * L;
+            deltag[wrow + q] = my_delta;
+            lse2g[wrow + q] = lse2;
+        }
+    };
 
     int roff[KK], toff[DB][2];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk)
         roff[kk] = tile_off<D>(l32, kk * 16 + g * 8);
     {
-        const int G = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
+        const int G16 = lane >> 4, e = (lane & 15) >> 2, c = lane & 3;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int hh = 0; hh < 2; ++hh)
-                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G & 1) + 4 * c);
+                toff[db][hh] = tile_off<D>(8 * hh + 4 * g + e, db * 32 + 16 * (G16 & 1) + 4 * c);
     }
 
     f32x16 dq[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-        dq[db] = f32x16{};
-
     DmaPlan<D, T::BN, 4> plan;
     plan.init(rs, wave, lane);
-    auto issue = [&](int t, uint16_t *stage) {
-        plan.issue(stage, Kb, rs, t * T::BN, L, wave, lane);
-        plan.issue(stage + T::TILE, Vb, rs, t * T::BN, L, wave, lane);
+    auto issue = [&](const QItem &x, int t, uint16_t *stage) __attribute__((always_inline)) {
+        plan.issue(stage, K + x.base, rs, t * T::BN, L, wave, lane);
+        plan.issue(stage + T::TILE, V + x.base, rs, t * T::BN, L, wave, lane);
     };
 
     // One tile; MASKED selects the boundary-tile variant at compile time.
@@ -470,42 +508,94 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             body(j0, bufc, IC<1>{});
     };
 
-    issue(t_begin, lds);
-    wait_vmem();
-    __syncthreads();
-    for (int t = t_begin;;) {
-        if (t < t_end)
-            issue(t + 1, lds + T::STAGE);
-        compute(t, IC<0>{});
-        wait_vmem();
-        __syncthreads();
-        if (t == t_end)
-            break;
-        ++t;
-        if (t < t_end)
-            issue(t + 1, lds);
-        compute(t, IC<1>{});
-        wait_vmem();
-        __syncthreads();
-        if (t == t_end)
-            break;
-        ++t;
-    }
+    // dQ (scaled, and with respect to the unrotated queries under RoPE) of
+    // the current item.
+    auto store = [&]() __attribute__((always_inline)) {
+        if (!q_ok)
+            return;
+        if (rope != 0) {
+            // Keeps the frequency arithmetic here: hoisted out of the item
+            // loop it would hold registers across every tile.
+            int gl = g;
+            RopeEpi r = rt;
+            asm volatile("" : "+v"(gl), "+s"(r.p0), "+s"(r.p1), "+s"(r.p2), "+s"(r.p3),
+                         "+s"(r.r4), "+s"(r.r16));
+            rope_unrotate_acc<DB>(dq, r, rope_position(it.b, L, my_q, cu, n_docs, rope), gl);
+        }
+        uint16_t *dQb = dQ + it.base + my_q * rs;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+                const int d = db * 32 + 8 * rg + 4 * g;
+                *reinterpret_cast<bf16x4 *>(dQb + d) =
+                    pack4(dq[db][4 * rg] * scale, dq[db][4 * rg + 1] * scale,
+                          dq[db][4 * rg + 2] * scale, dq[db][4 * rg + 3] * scale);
+            }
+    };
 
-    if (!q_ok)
-        return;
-    if (rope != 0)  // dQ with respect to the unrotated queries
-        rope_unrotate_acc<DB>(dq, rt, rope_position(b, L, my_q, cu, n_docs, rope), g);
-    uint16_t *dQb = dQ + base + my_q * rs;
+    setup(it);
+    load_rows(it);
+    finish_rows(it);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-            const int d = db * 32 + 8 * rg + 4 * g;
-            *reinterpret_cast<bf16x4 *>(dQb + d) =
-                pack4(dq[db][4 * rg] * scale, dq[db][4 * rg + 1] * scale,
-                      dq[db][4 * rg + 2] * scale, dq[db][4 * rg + 3] * scale);
+        dq[db] = f32x16{};
+    int t = it.t_begin;
+    issue(it, t, lds);
+    wait_vmem();
+    __syncthreads();
+
+    // One key tile in LDS stage BUF; the next tile (of this item or the next
+    // one) goes to the other stage.  Returns false after the last item.
+    auto step = [&](auto bufc) __attribute__((always_inline)) -> bool {
+        constexpr int BUF = decltype(bufc)::value;
+        uint16_t *other = lds + (1 - BUF) * T::STAGE;
+        const bool last = t == it.t_end;
+        bool more = false;
+        if (!last) {
+            issue(it, t + 1, other);
+        } else if constexpr (PERSIST) {
+            const int nbid = item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
+            more = nbid >= 0;
+            if (more) {
+                nit = q_item<D>(nbid, nqb, B, L, H, causal, cu, n_docs);
+                issue(nit, nit.t_begin, other);
+            }
         }
+        compute(t, bufc);
+        if (more)  // Q, dO, O rows of the next item (registers free after the tile)
+            load_rows(nit);
+        wait_vmem();
+        __syncthreads();
+        if (!last) {
+            ++t;
+            return true;
+        }
+        if constexpr (!PERSIST) {
+            return false;  // stored after the loop
+        } else {
+            store();
+            if (!more)
+                return false;
+        }
+        ++k_item;
+        it = nit;
+        setup(it);
+        finish_rows(it);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+            dq[db] = f32x16{};
+        t = it.t_begin;
+        return true;
+    };
+    for (;;) {
+        if (!step(IC<0>{}))
+            break;
+        if (!step(IC<1>{}))
+            break;
+    }
+    if constexpr (!PERSIST)
+        store();
 }
 
 // Explicit instantiations: the host-side launch stubs of these kernel
@@ -523,8 +613,9 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const int32_t *__restrict__, int, float, float, int, RopeEpi, int
 template __global__ void dkdv1_kernel<64, false>(DD_KV_ARGS);  // D = 64: single-role waves
 template __global__ void dkdv1_kernel<64, true>(DD_KV_ARGS);
-template __global__ void dq_kernel<64>(DD_Q_ARGS);
-template __global__ void dq_kernel<128>(DD_Q_ARGS);
+template __global__ void dq_kernel<64, false>(DD_Q_ARGS);
+template __global__ void dq_kernel<64, true>(DD_Q_ARGS);  // D = 128: never persistent
+template __global__ void dq_kernel<128, false>(DD_Q_ARGS);
 #undef DD_KV_ARGS
 #undef DD_Q_ARGS
 
@@ -549,9 +640,22 @@ static int launch_bwd_d(const BwdArgs &a)
     hipError_t e;
     const int nqb = (a.L + QTile<D>::BM - 1) / QTile<D>::BM;
     {
+        const long long all =
+            (static_cast<long long>(nqb) * a.B * a.H + kXcds - 1) / kXcds * kXcds;
+        // Persistent only at D = 64: at D = 128 its item loop spills.
+        long long pgrid = 0;
+        if constexpr (D == 64)
+            if (doc_span_tokens(a) <= kDqPersistMaxSpan)
+                pgrid = persistent_grid<dq_kernel<D, true>>(256);
+        const bool persist = pgrid > 0 && pgrid < all;
+        auto kern = dq_kernel<D, false>;
+        if constexpr (D == 64)
+            if (persist)
+                kern = dq_kernel<D, true>;
         ProfScope prof(K_DQ, st);
-        e = launch_kernel(dq_kernel<D>, dim3(static_cast<unsigned>(nqb * a.B * a.H)), dim3(256),
-                          st, a.Q, a.K, a.V, a.O, a.dO, a.LSE, lse2, delta, a.dQ, a.B, a.L, a.H,
+        e = launch_kernel(kern,
+                          dim3(static_cast<unsigned>(persist ? pgrid : all)), dim3(256), st, a.Q,
+                          a.K, a.V, a.O, a.dO, a.LSE, lse2, delta, a.dQ, a.B, a.L, a.H,
                           a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale, nqb, s.rt,
                           s.rope);
     }

@@ -293,8 +293,10 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             // Keeps the frequency arithmetic here: hoisted out of the item
             // loop it would hold ~24 registers across every tile.
             int gl = g;
-            asm volatile("" : "+v"(gl));
-            rope_unrotate_acc<DB>(acc, rt, rope_position(it.b, L, my_k, cu, n_docs, rope), gl);
+            RopeEpi r = rt;
+            asm volatile("" : "+v"(gl), "+s"(r.p0), "+s"(r.p1), "+s"(r.p2), "+s"(r.p3),
+                         "+s"(r.r4), "+s"(r.r16));
+            rope_unrotate_acc<DB>(acc, r, rope_position(it.b, L, my_k, cu, n_docs, rope), gl);
         }
         const float osc = role_a ? 1.0f : scale;
         uint16_t *dst = (role_a ? dV : dK) + it.base + my_k * rs;
@@ -344,9 +346,13 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             ++t;
             return true;
         }
-        store();
-        if (!PERSIST || !more)
-            return false;
+        if constexpr (!PERSIST) {
+            return false;  // stored after the loop
+        } else {
+            store();
+            if (!more)
+                return false;
+        }
         ++k_item;
         it = nit;
         setup(it);
@@ -362,6 +368,8 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         if (!step(IC<1>{}))
             break;
     }
+    if constexpr (!PERSIST)
+        store();
 }
 
 #define DD_KV_ARGS                                                                               \

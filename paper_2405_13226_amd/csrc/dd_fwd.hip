@@ -312,9 +312,13 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             ++t;
             return true;
         }
-        store();
-        if (!PERSIST || !more)
-            return false;
+        if constexpr (!PERSIST) {
+            return false;  // stored after the loop
+        } else {
+            store();
+            if (!more)
+                return false;
+        }
         ++k_item;
         it = nit;
         setup(it);
@@ -328,6 +332,8 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         if (!step(IC<1>{}))
             break;
     }
+    if constexpr (!PERSIST)
+        store();
 }
 
 // Explicit instantiations: the host-side launch stubs are emitted here
