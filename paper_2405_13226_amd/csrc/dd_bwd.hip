@@ -293,7 +293,8 @@ struct QTile {
     static constexpr int STAGE = 2 * TILE; // K then V
 };
 
-// Spans (tokens) up to which dQ runs persistently (D = 64).
+// Row lengths (tokens) up to which dQ runs persistently (D = 64); as for
+// dK/dV the test ignores document masking.
 constexpr long long kDqPersistMaxSpan = 2048;
 
 // A query-block work item of the dQ kernel: one block of QTile::BM queries
@@ -324,7 +325,7 @@ __device__ __forceinline__ QItem q_item(int bid, int nqb, int B, int L, int H, b
 }
 
 // PERSIST = false: one query block per workgroup.  PERSIST = true (short
-// spans, D = 64 only; at D = 128 the item loop spills): a workgroup walks
+// rows, D = 64 only; at D = 128 the item loop spills): a workgroup walks
 // its query blocks in the order of item_bid;
 // during a block's last key tile it DMAs the next block's first K/V tile
 // into the free stage, and right after that tile loads the next block's Q,
@@ -645,7 +646,7 @@ static int launch_bwd_d(const BwdArgs &a)
         // Persistent only at D = 64: at D = 128 its item loop spills.
         long long pgrid = 0;
         if constexpr (D == 64)
-            if (doc_span_tokens(a) <= kDqPersistMaxSpan)
+            if (a.L <= kDqPersistMaxSpan)
                 pgrid = persistent_grid<dq_kernel<D, true>>(256);
         const bool persist = pgrid > 0 && pgrid < all;
         auto kern = dq_kernel<D, false>;
@@ -669,9 +670,9 @@ static int launch_bwd_d(const BwdArgs &a)
             const int nkb = (a.L + T::BN - 1) / T::BN;
             const long long n_items = static_cast<long long>(nkb) * a.B * a.H;
             const long long all = (n_items + kXcds - 1) / kXcds * kXcds;
-            // Persistent for short spans, as many workgroups as are resident
+            // Persistent for short rows, as many workgroups as are resident
             // at once (two per CU).
-            const long long pgrid = doc_span_tokens(a) <= kPersistMaxSpan
+            const long long pgrid = a.L <= kPersistMaxSpan
                                         ? persistent_grid<dkdv1_kernel<D, true>>(64 * T::NW)
                                         : 0;
             const bool persist = pgrid > 0 && pgrid < all;

@@ -25,20 +25,14 @@ struct BwdScalars {
 // runtime's launch status.
 hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s);
 
-// Below this many tokens per document span (the row, or the mean document
-// length under document masking) a key block visits few query tiles, and the
-// persistent dK/dV forms, which hide each item's set-up behind the previous
-// item, are faster; above it the items are long and one item per workgroup
-// (hardware dispatch) is.
+// Rows of at most this many tokens take the persistent dK/dV forms: a key
+// block then visits few query tiles, and a workgroup that walks its blocks
+// back to back hides each block's set-up behind the previous one; longer
+// rows have long items and run one item per workgroup (hardware dispatch).
+// The test is on the row length even under document masking: documents make
+// the work per block uneven, which the hardware's dispatch balances and the
+// persistent forms' fixed order does not.
 constexpr long long kPersistMaxSpan = 1024;
-
-inline long long doc_span_tokens(const BwdArgs &a)
-{
-    if (!a.cu || a.n_docs < 1)
-        return a.L;
-    const long long mean = static_cast<long long>(a.B) * a.L / a.n_docs;
-    return mean < a.L ? mean : a.L;
-}
 
 // ---------------------------------------------------------------------------
 // Work items of the persistent dK/dV kernels

@@ -407,9 +407,8 @@ hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s)
     const int nkb = (a.L + T::BN - 1) / T::BN;
     const long long n_items = static_cast<long long>(nkb) * a.B * a.H;
     const long long all = (n_items + kXcds - 1) / kXcds * kXcds;
-    const long long span = doc_span_tokens(a);
     hipStream_t st = static_cast<hipStream_t>(a.stream);
-    if (span > kPersistMaxSpan)
+    if (a.L > kPersistMaxSpan)
         return launch_kernel(dkdv_kernel<128, false>, dim3(static_cast<unsigned>(all)),
                              dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.delta, a.dK,
                              a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2,

@@ -41,7 +41,9 @@ struct FwdTile {
 // unchanged.
 constexpr float kRescaleSlack = 8.0f;
 
-// Spans (tokens) up to which the forward runs persistently.
+// Row lengths (tokens) up to which the forward runs persistently.  The test
+// ignores document masking: documents make the work per query block uneven,
+// which hardware dispatch balances and a fixed walk order does not.
 constexpr long long kFwdPersistMaxSpan = 2048;
 
 // A query-block work item of the forward: one block of FwdTile::BM queries of
@@ -73,7 +75,7 @@ __device__ __forceinline__ FwdItem fwd_item(int bid, int nqb, int B, int L, int 
 }
 
 // PERSIST = false: one query block per workgroup.  PERSIST = true (short
-// spans): a workgroup walks its query blocks in the order of item_bid; during
+// rows): a workgroup walks its query blocks in the order of item_bid; during
 // a block's last key tile it DMAs the next block's first K/V tile into the
 // free stage, and after that tile loads the next block's Q rows.
 template <int D, bool PERSIST>
@@ -355,12 +357,8 @@ static int launch_fwd_d(const FwdArgs &a)
     const int nqb = (a.L + FwdTile<D>::BM - 1) / FwdTile<D>::BM;
     const long long all = (static_cast<long long>(nqb) * a.B * a.H + kXcds - 1) / kXcds * kXcds;
     const float scale_log2 = kLog2e / sqrtf(static_cast<float>(D));
-    // Persistent for short spans (the row, or the mean document length under
-    // document masking): as many workgroups as are resident at once.
-    const long long span =
-        a.cu && a.n_docs > 0 ? std::min<long long>(a.L, static_cast<long long>(a.B) * a.L / a.n_docs)
-                             : a.L;
-    const long long pgrid = span <= kFwdPersistMaxSpan ? persistent_grid<fwd_kernel<D, true>>(256) : 0;
+    // Persistent for short rows: as many workgroups as are resident at once.
+    const long long pgrid = a.L <= kFwdPersistMaxSpan ? persistent_grid<fwd_kernel<D, true>>(256) : 0;
     const bool persist = pgrid > 0 && pgrid < all;
     ProfScope prof(K_FWD, static_cast<hipStream_t>(a.stream));
     const hipError_t e = launch_kernel(
