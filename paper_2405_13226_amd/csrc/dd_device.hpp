@@ -148,6 +148,25 @@ __device__ __forceinline__ int item_bid(int k, int w, int G, int n_items)
     return bid < n_items ? bid : -1;
 }
 
+// Reductions over the two halves of a wave (lanes l and l ^ 32), with
+// v_permlane32_swap: called with two copies of v, it returns one copy whose
+// upper half received the lower half's values and one whose lower half
+// received the upper half's, i.e. {v[l % 32], v[l % 32 + 32]} in every lane l.
+// A VALU exchange, no LDS round trip; max and + are symmetric, so the result
+// is the same in both halves.
+__device__ __forceinline__ float halves_max(float v)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float v)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Wave-wide min / max of an int.
 __device__ __forceinline__ int wave_min(int v)
 {

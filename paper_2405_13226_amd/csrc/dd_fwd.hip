@@ -189,13 +189,14 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     s[kb][r] = ok ? s[kb][r] : -INFINITY;
                 }
         }
-        float mx = -INFINITY;
+        // Four independent chains (max is exact, so the order is free).
+        float m4[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-                mx = fmaxf(mx, s[kb][r]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+                m4[r & 3] = fmaxf(m4[r & 3], s[kb][r]);
+        const float mx = halves_max(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
         const float mc = mx * scale_log2;  // log2-domain tile maximum
 
         // Lazy rescale: only when some lane's maximum grew past the slack.
@@ -256,7 +257,7 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     auto store = [&]() __attribute__((always_inline)) {
         if (!q_ok)
             return;
-        const float l_tot = l_i + __shfl_xor(l_i, 32);
+        const float l_tot = halves_sum(l_i);
         const float inv = 1.0f / l_tot;
         uint16_t *Ob = O + it.base + my_q * rs;
 #pragma unroll

@@ -10,7 +10,7 @@ import pytest
 import synth
 from paper_2405_13226_amd import dd
 
-from parity import check_case, log
+from parity import assert_ok, check_case, compare, gpu_run, log
 
 pytestmark = pytest.mark.gpu
 
@@ -62,6 +62,27 @@ def test_persistent_kernels_document_masked(cuda, D):
     cu = dd.chunk_doclens(lens, B * L)
     check_case(B, L, H, D, causal=True, cu=cu, seed=12, bh=bh,
                tag=f"persistent D={D}, documents")
+
+
+@pytest.mark.parametrize("B,L,D,causal", [(2, 700, 64, True), (2, 700, 128, False),
+                                         (1, 2100, 64, True), (1, 2100, 128, True)])
+def test_large_scores_forward(cuda, B, L, D, causal):
+    # Q and K times 8 (exact in bf16): the scaled scores in log2 units reach
+    # several hundred, far outside exp2's fp32 range, so each tile's running
+    # maximum must be the true maximum of its rows (a smaller one overflows
+    # the probabilities, a larger one underflows their sum).  L = 700 takes
+    # the persistent forward, L = 2100 one block per workgroup.
+    H = 2
+    inputs = synth.attention_inputs(B, L, H, D, seed=21 + D, with_grad=False)
+    for n in ("q", "k"):
+        inputs[n] = synth.bf16_bits_from_f32(synth.f32_from_bf16_bits(inputs[n]) * 8.0)
+    log(f"case large scores B={B} L={L} D={D} causal={int(causal)}")
+    out = gpu_run(inputs, causal, None, "cuda:0", backward=False)
+    for n, t in out.items():
+        assert bool(np.isfinite(t.float().cpu().numpy()).all()), f"{n} has non-finite values"
+    bh = [(b, h) for b in range(B) for h in range(H)]
+    res = compare(inputs, out, causal, None, bh, backward=False, tag="large scores")
+    assert_ok(res, backward=False)
 
 
 def test_single_token_documents(cuda):
