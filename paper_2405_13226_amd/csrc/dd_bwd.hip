@@ -5,8 +5,8 @@
 //   1. dq:    query-resident.  One workgroup = 4 waves = 128 queries; each
 //             wave keeps its queries' Q and dO rows in registers.  It first
 //             forms delta_i = sum_d dO_id O_id and the LSE in log2 units for
-//             its queries and writes both, fp32, to a [B*H][L] workspace (one
-//             contiguous row per (b, h)); then it walks the key tiles (64
+//             its queries and writes -delta and the LSE, fp32, to a [B*H][L]
+//             workspace (one contiguous row per (b, h)); then it walks the key tiles (64
 //             keys) its queries see and forms
 //               S^T = K Q^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T,
 //             with K and V tiles in LDS (K^T read transposed).
@@ -15,10 +15,10 @@
 //             V (the other) rows in registers; for D = 64 (here) one wave
 //             holds both.  They walk the query tiles (64 queries) their keys
 //             are visible to and form
-//               S = Q K^T, P = exp2(S*scale*log2e - lse2), dP = dO V^T,
-//               dS = P * (dP - delta),
+//               S = Q K^T, P = exp2(S*scale*log2e - lse2),
+//               dP - delta = dO V^T accumulated onto -delta,  dS = P (dP - delta),
 //               dV^T += dO^T P,  dK^T += Q^T dS,
-//             reading lse2 and delta of each tile from the workspace.
+//             reading lse2 and -delta of each tile from the workspace.
 //             Q and dO tiles arrive row-major in LDS by direct DMA; S and dP
 //             read them row-wise, dV^T and dK^T transposed (ds_read_b64_tr_b16).
 // Splitting dQ from dK/dV keeps every output owned by exactly one workgroup:
@@ -58,7 +58,7 @@ template <int D, bool PERSIST>
 __global__ void __launch_bounds__(256, 2)
 dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
              const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
-             const float *__restrict__ lse2g, const float *__restrict__ deltag,
+             const float *__restrict__ lse2g, const float *__restrict__ ndeltag,
              uint16_t *__restrict__ dK, uint16_t *__restrict__ dV, int B, int L, int H,
              int causal_i, const int32_t *__restrict__ cu, int n_docs, float scale_log2,
              float scale, int nkb, RopeEpi rt, int rope)
@@ -138,11 +138,21 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const uint16_t *qs = lds + BUF * T::STAGE;
         const uint16_t *dos = qs + T::TILE;
         const float *lse_s = reinterpret_cast<const float *>(qs + 2 * T::TILE);
-        const float *dlt_s = lse_s + T::BM;
+        const float *ndl_s = lse_s + T::BM;
         const int qlo_r = qlo_k - i0 - 4 * g, qhi_r = qhi_k - i0 - 4 * g;
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-            f32x16 s = f32x16{}, dp = f32x16{};
+            // dP accumulates onto -delta of its rows (C layout: register
+            // 4*rg + e holds query 8*rg + 4*g + e), so the products give
+            // dP - delta directly.
+            f32x16 s = f32x16{}, dp;
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+                const f32x4 nz = *reinterpret_cast<const f32x4 *>(ndl_s + qb * 32 + 8 * rg + 4 * g);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    dp[4 * rg + e] = nz[e];
+            }
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
                 const int off = qb * 32 * D + roff[kk];
@@ -153,7 +163,6 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             for (int rg = 0; rg < 4; ++rg) {
                 const int ql = qb * 32 + 8 * rg + 4 * g;
                 const f32x4 lz = *reinterpret_cast<const f32x4 *>(lse_s + ql);
-                const f32x4 dz = *reinterpret_cast<const f32x4 *>(dlt_s + ql);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int r = 4 * rg + e;
@@ -164,7 +173,7 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                         p = ok ? p : 0.f;
                     }
                     s[r] = p;
-                    dp[r] = p * (dp[r] - dz[e]);
+                    dp[r] = p * dp[r];
                 }
             }
 #pragma unroll
@@ -229,7 +238,7 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         dv[db] = f32x16{};
     }
     int t = it.t_begin;
-    kv_issue<D, T>(plan, lds, Q, dO, lse2g, deltag, it, t, L, rs, wave, lane);
+    kv_issue<D, T>(plan, lds, Q, dO, lse2g, ndeltag, it, t, L, rs, wave, lane);
     wait_vmem();
     __syncthreads();
 
@@ -241,13 +250,13 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const bool last = t == it.t_end;
         bool more = false;
         if (!last) {
-            kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, it, t + 1, L, rs, wave, lane);
+            kv_issue<D, T>(plan, other, Q, dO, lse2g, ndeltag, it, t + 1, L, rs, wave, lane);
         } else if constexpr (PERSIST) {
             const int nbid = item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
             more = nbid >= 0;
             if (more) {
                 nit = kv_item<D, T>(nbid, nkb, B, L, H, causal, cu, n_docs);
-                kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, nit, nit.t_begin, L, rs, wave,
+                kv_issue<D, T>(plan, other, Q, dO, lse2g, ndeltag, nit, nit.t_begin, L, rs, wave,
                                lane);
             }
         }
@@ -335,7 +344,7 @@ __global__ void __launch_bounds__(256, 2)
 dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
           const uint16_t *__restrict__ V, const uint16_t *__restrict__ O,
           const uint16_t *__restrict__ dO, const float *__restrict__ LSE,
-          float *__restrict__ lse2g, float *__restrict__ deltag,
+          float *__restrict__ lse2g, float *__restrict__ ndeltag,
           uint16_t *__restrict__ dQ, int B, int L, int H, int causal_i,
           const int32_t *__restrict__ cu, int n_docs, float scale_log2, float scale, int nqb,
           RopeEpi rt, int rope)
@@ -410,7 +419,7 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         neg_lse2 = -lse2;
         if (q < L && g == 0) {
             const long long wrow = static_cast<long long>(x.bh) * L;
-            deltag[wrow + q] = my_delta;
+            ndeltag[wrow + q] = -my_delta;
             lse2g[wrow + q] = lse2;
         }
     };
@@ -615,8 +624,8 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 template __global__ void dkdv1_kernel<64, false>(DD_KV_ARGS);  // D = 64: single-role waves
 template __global__ void dkdv1_kernel<64, true>(DD_KV_ARGS);
 template __global__ void dq_kernel<64, false>(DD_Q_ARGS);
-template __global__ void dq_kernel<64, true>(DD_Q_ARGS);  // D = 128: never persistent
-template __global__ void dq_kernel<128, false>(DD_Q_ARGS);
+template __global__ void dq_kernel<64, true>(DD_Q_ARGS);
+template __global__ void dq_kernel<128, false>(DD_Q_ARGS);  // D = 128: never persistent
 #undef DD_KV_ARGS
 #undef DD_Q_ARGS
 
@@ -627,17 +636,17 @@ static int launch_bwd_d(const BwdArgs &a)
     hipStream_t st = static_cast<hipStream_t>(a.stream);
     const size_t region = align256(static_cast<size_t>(a.B) * a.H * a.L * sizeof(float));
     float *lse2 = static_cast<float *>(a.workspace);
-    float *delta = reinterpret_cast<float *>(static_cast<char *>(a.workspace) + region);
+    float *ndelta = reinterpret_cast<float *>(static_cast<char *>(a.workspace) + region);
     BwdScalars s;
     s.lse2 = lse2;
-    s.delta = delta;
+    s.ndelta = ndelta;
     s.scale = 1.0f / sqrtf(static_cast<float>(D));
     s.scale_log2 = s.scale * kLog2e;
     // RoPE: 0 off, 1 row positions, 2 document-local positions.
     s.rope = a.rope_base > 0.0 ? (a.rope_doc && a.cu ? 2 : 1) : 0;
     s.rt = s.rope ? rope_epi(a.rope_base, D) : RopeEpi{};
 
-    // dQ first: it also writes delta and log2-LSE, which dK/dV reads.
+    // dQ first: it also writes -delta and log2-LSE, which dK/dV reads.
     hipError_t e;
     const int nqb = (a.L + QTile<D>::BM - 1) / QTile<D>::BM;
     {
@@ -656,7 +665,7 @@ static int launch_bwd_d(const BwdArgs &a)
         ProfScope prof(K_DQ, st);
         e = launch_kernel(kern,
                           dim3(static_cast<unsigned>(persist ? pgrid : all)), dim3(256), st, a.Q,
-                          a.K, a.V, a.O, a.dO, a.LSE, lse2, delta, a.dQ, a.B, a.L, a.H,
+                          a.K, a.V, a.O, a.dO, a.LSE, lse2, ndelta, a.dQ, a.B, a.L, a.H,
                           a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale, nqb, s.rt,
                           s.rope);
     }
@@ -679,7 +688,7 @@ static int launch_bwd_d(const BwdArgs &a)
             auto kern = persist ? dkdv1_kernel<D, true> : dkdv1_kernel<D, false>;
             const long long grid = persist ? pgrid : all;
             e = launch_kernel(kern, dim3(static_cast<unsigned>(grid)), dim3(64 * T::NW), st, a.Q,
-                              a.K, a.V, a.dO, lse2, delta, a.dK, a.dV, a.B, a.L, a.H,
+                              a.K, a.V, a.dO, lse2, ndelta, a.dK, a.dV, a.B, a.L, a.H,
                               a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale, nkb, s.rt,
                               s.rope);
         } else {

@@ -14,7 +14,7 @@ namespace dd {
 // Per-call values every backward kernel takes, derived once by the launcher.
 struct BwdScalars {
     const float *lse2;   // [B*H][L] log-sum-exp in log2 units (workspace)
-    const float *delta;  // [B*H][L] rowsum(dO * O) (workspace)
+    const float *ndelta; // [B*H][L] -rowsum(dO * O) (workspace)
     float scale_log2;    // softmax scale times log2(e)
     float scale;         // softmax scale 1/sqrt(D)
     RopeEpi rt;          // rotary frequencies for the dQ / dK epilogues
@@ -64,14 +64,14 @@ __device__ __forceinline__ KvItem kv_item(int bid, int nkb, int B, int L, int H,
 }
 
 // Direct-to-LDS loads of query tile t of item x into `stage`: the Q and dO
-// tiles (T::TILE elements each), then lse2 and delta of its rows (waves 0
+// tiles (T::TILE elements each), then lse2 and -delta of its rows (waves 0
 // and 1).
 template <int D, class T>
 __device__ __forceinline__ void kv_issue(const DmaPlan<D, T::BM, T::NW> &plan, uint16_t *stage,
                                          const uint16_t *__restrict__ Q,
                                          const uint16_t *__restrict__ dO,
                                          const float *__restrict__ lse2g,
-                                         const float *__restrict__ deltag, const KvItem &x, int t,
+                                         const float *__restrict__ ndeltag, const KvItem &x, int t,
                                          int L, long long rs, int wave, int lane)
 {
     const int i0 = t * T::BM;
@@ -81,7 +81,7 @@ __device__ __forceinline__ void kv_issue(const DmaPlan<D, T::BM, T::NW> &plan, u
     if (wave == 0)
         dma_row_f32(fs, lse2g + static_cast<long long>(x.bh) * L, i0, L, lane);
     else if (wave == 1)
-        dma_row_f32(fs + T::BM, deltag + static_cast<long long>(x.bh) * L, i0, L, lane);
+        dma_row_f32(fs + T::BM, ndeltag + static_cast<long long>(x.bh) * L, i0, L, lane);
 }
 
 

@@ -19,7 +19,7 @@ struct KvTile {
     static constexpr int BM = 64;             // queries per tile
     static constexpr int NW = 8;              // waves: 4 key groups x 2 roles
     static constexpr int TILE = BM * D;       // elements of a Q or dO tile
-    // Q tile, dO tile, then lse2[BM] and delta[BM] as floats.
+    // Q tile, dO tile, then lse2[BM] and -delta[BM] as floats.
     static constexpr int STAGE = 2 * TILE + 2 * BM * 2;
     // P hand-off between the two waves of a key group: per group, 32 fp32
     // per lane (two 32-query blocks x 16 C-layout registers), 8 KiB.
@@ -37,7 +37,8 @@ constexpr int kAhead = 4;
 //   role A (waves 0-3): K in registers; S = Q K^T, P = exp2(S*c - lse2)
 //                       (masked), P handed to role B through LDS,
 //                       dV^T += dO^T P;
-//   role B (waves 4-7): V in registers; dP = dO V^T, then dS = P (dP - delta),
+//   role B (waves 4-7): V in registers; dP - delta = dO V^T accumulated onto
+//   -delta, then dS = P (dP - delta),
 //                       dK^T += Q^T dS.
 // Each wave holds one accumulator set, so two waves fit per SIMD and one
 // wave's softmax arithmetic overlaps the other's matrix products.
@@ -53,7 +54,7 @@ template <int D, bool PERSIST>
 __global__ void __launch_bounds__(512, 1)
 dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
-            const float *__restrict__ lse2g, const float *__restrict__ deltag,
+            const float *__restrict__ lse2g, const float *__restrict__ ndeltag,
             uint16_t *__restrict__ dK, uint16_t *__restrict__ dV, int B, int L, int H,
             int causal_i, const int32_t *__restrict__ cu, int n_docs, float scale_log2,
             float scale, int nkb, RopeEpi rt, int rope)
@@ -166,9 +167,8 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     // Row-wise products X K^T (role A, X = Q) or X V^T (role B, X = dO).
     // The two 32-query blocks' chains alternate; same issue order as above,
     // one read per product.
+    // c[qb] += (tile rows qb*32..qb*32+31) . (this wave's register rows)^T.
     auto row_products = [&](const uint16_t *tile, f32x16 (&c)[2]) {
-        c[0] = f32x16{};
-        c[1] = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
@@ -193,7 +193,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const uint16_t *qs = lds + BUF * T::STAGE;
         const uint16_t *dos = qs + T::TILE;
         const float *lse_s = reinterpret_cast<const float *>(qs + 2 * T::TILE);
-        const float *dlt_s = lse_s + T::BM;
+        const float *ndl_s = lse_s + T::BM;
         f32x16 c[2];
         bf16x8 bop[2][2];
         if (role_a) {
@@ -207,6 +207,8 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     __builtin_amdgcn_s_setprio(3);
                     __builtin_amdgcn_sched_barrier(0);
                 }
+                c[0] = f32x16{};
+                c[1] = f32x16{};
                 row_products(qs, c);
                 if constexpr (PERSIST) {
                     __builtin_amdgcn_sched_barrier(0);
@@ -241,8 +243,23 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                         bop[qb][t2] = pack8(c[qb], 8 * t2);
             }
         } else {
-            if (active)
-                row_products(dos, c);  // dP
+            if (active) {
+                // dP accumulates onto -delta of its rows (register 4*rg + e
+                // holds query qb*32 + 8*rg + 4*g + e): the products give
+                // dP - delta directly.
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+                    for (int rg = 0; rg < 4; ++rg) {
+                        const f32x4 nz = *reinterpret_cast<const f32x4 *>(
+                            ndl_s + qb * 32 + 8 * rg + 4 * g);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            c[qb][4 * rg + e] = nz[e];
+                    }
+                __builtin_amdgcn_sched_barrier(0);
+                row_products(dos, c);
+            }
         }
         __syncthreads();  // P visible to role B
         if (reload)
@@ -256,12 +273,10 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                 for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
                     for (int rg = 0; rg < 4; ++rg) {
-                        const f32x4 dz = *reinterpret_cast<const f32x4 *>(
-                            dlt_s + qb * 32 + 8 * rg + 4 * g);
                         const f32x4 pv = *reinterpret_cast<const f32x4 *>(pslot + (qb * 4 + rg) * 256);
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            c[qb][4 * rg + e] = pv[e] * (c[qb][4 * rg + e] - dz[e]);
+                            c[qb][4 * rg + e] = pv[e] * c[qb][4 * rg + e];
                     }
 #pragma unroll
                 for (int qb = 0; qb < 2; ++qb)
@@ -317,7 +332,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     for (int db = 0; db < DB; ++db)
         acc[db] = f32x16{};
     int t = it.t_begin;
-    kv_issue<D, T>(plan, lds, Q, dO, lse2g, deltag, it, t, L, rs, wave, lane);
+    kv_issue<D, T>(plan, lds, Q, dO, lse2g, ndeltag, it, t, L, rs, wave, lane);
     wait_vmem();
     __syncthreads();
 
@@ -329,13 +344,13 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const bool last = t == it.t_end;
         bool more = false;
         if (!last) {
-            kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, it, t + 1, L, rs, wave, lane);
+            kv_issue<D, T>(plan, other, Q, dO, lse2g, ndeltag, it, t + 1, L, rs, wave, lane);
         } else if constexpr (PERSIST) {
             const int nbid = item_bid(k_item + 1, static_cast<int>(blockIdx.x), G, n_items);
             more = nbid >= 0;
             if (more) {
                 nit = kv_item<D, T>(nbid, nkb, B, L, H, causal, cu, n_docs);
-                kv_issue<D, T>(plan, other, Q, dO, lse2g, deltag, nit, nit.t_begin, L, rs, wave,
+                kv_issue<D, T>(plan, other, Q, dO, lse2g, ndeltag, nit, nit.t_begin, L, rs, wave,
                                  lane);
             }
         }
@@ -410,7 +425,7 @@ hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s)
     hipStream_t st = static_cast<hipStream_t>(a.stream);
     if (a.L > kPersistMaxSpan)
         return launch_kernel(dkdv_kernel<128, false>, dim3(static_cast<unsigned>(all)),
-                             dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.delta, a.dK,
+                             dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.ndelta, a.dK,
                              a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2,
                              s.scale, nkb, s.rt, s.rope);
     // Persistent: as many workgroups as are resident at once (one per CU).
@@ -419,7 +434,7 @@ hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s)
         return hipErrorInvalidDevice;
     const long long grid = std::min(pgrid, all);
     return launch_kernel(dkdv_kernel<128, true>, dim3(static_cast<unsigned>(grid)),
-                         dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.delta, a.dK, a.dV,
+                         dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.ndelta, a.dK, a.dV,
                          a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale,
                          nkb, s.rt, s.rope);
 }
