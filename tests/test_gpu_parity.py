@@ -39,12 +39,14 @@ def test_document_masked_chunks(cuda, D, causal):
     check_case(B, L, H, D, causal=causal, cu=cu, seed=D + causal)
 
 
-# Short spans take the persistent forms of the forward and dK/dV kernels,
-# where a workgroup walks several blocks back to back.  Grids: forward 768
-# (D = 64) / 512 (D = 128) workgroups, dK/dV 512 / 256.  48 x 3 slices of
+# Short rows take the persistent forms of the forward, dK/dV and (D = 64) dQ
+# kernels, where a workgroup walks several blocks back to back.  Grids:
+# forward 768 (D = 64) / 512 (D = 128) workgroups, dK/dV 512 / 256, dQ 512
+# (D = 64).  48 x 3 slices of
 # L = 700 hold 6 query blocks and 6 key blocks each (864 of each), so the last
 # slices fall in a workgroup's second (or later) item; the last block of every
-# slice holds 60 rows (ragged).  With documents the span is their mean length.
+# slice holds 60 rows (ragged).  The choice follows the row length, so the
+# document-masked case takes the same persistent forms.
 PERSIST_CASES = {128: (48, [(0, 0), (15, 1), (31, 0), (40, 2), (47, 2)]),
                  64: (48, [(0, 0), (15, 1), (31, 0), (40, 2), (47, 2)])}
 
