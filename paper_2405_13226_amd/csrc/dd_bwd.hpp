@@ -1,5 +1,5 @@
 // dd_bwd.hpp -- pieces of the attention backward shared by its translation
-// units (dd_bwd.hip: prep, dK/dV for D = 64, dQ and the launcher;
+// units (dd_bwd.hip: dK/dV for D = 64, dQ and the launcher;
 // dd_dkdv.hip: dK/dV for D = 128).
 #pragma once
 
