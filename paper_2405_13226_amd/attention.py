@@ -40,6 +40,12 @@ def _check_tensor(t, name, shape=None, dtype=torch.bfloat16):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
 
 
+def _empty(t) -> bool:
+    """B, L or H is 0: nothing to compute.  The C ABI takes each >= 1, so
+    the wrappers return empty results without calling it."""
+    return t.dim() == 4 and t.shape[0] * t.shape[1] * t.shape[2] == 0
+
+
 class DocLens:
     """Validated document offsets: a host copy and an int32 device copy."""
 
@@ -77,9 +83,11 @@ def forward(q, k, v, causal: bool = True, cu_doclens=None):
     B, L, H, D = q.shape
     _check_tensor(k, "k", q.shape)
     _check_tensor(v, "v", q.shape)
-    docs = _doclens(cu_doclens, B, L, q.device)
     o = torch.empty_like(q)
     lse = torch.empty((B, L, H), dtype=torch.float32, device=q.device)
+    if _empty(q):
+        return o, lse
+    docs = _doclens(cu_doclens, B, L, q.device)
     st = lib().dd_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, L, H, D,
                            int(bool(causal)), _ptr(docs.dev) if docs else None,
                            docs.n_docs if docs else 0, _stream(q.device))
@@ -98,11 +106,13 @@ def backward(q, k, v, o, lse, do, causal: bool = True, cu_doclens=None, workspac
     for t, n in ((k, "k"), (v, "v"), (o, "o"), (do, "do")):
         _check_tensor(t, n, q.shape)
     _check_tensor(lse, "lse", (B, L, H), torch.float32)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    if _empty(q):
+        return dq, dk, dv
     docs = _doclens(cu_doclens, B, L, q.device)
     need = workspace_bytes(B, L, H, D)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
-    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
     st = lib().dd_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
                            _ptr(dq), _ptr(dk), _ptr(dv), B, L, H, D, int(bool(causal)),
                            _ptr(docs.dev) if docs else None, docs.n_docs if docs else 0,
@@ -118,10 +128,12 @@ def rope(x, base: float, cu_doclens=None, doc_positions: bool = False, inverse: 
     ``out``, which may be ``x`` itself)."""
     _check_tensor(x, "x")
     B, L, H, D = x.shape
-    docs = _doclens(cu_doclens, B, L, x.device)
     y = torch.empty_like(x) if out is None else out
     if out is not None:
         _check_tensor(out, "out", x.shape)
+    if _empty(x):
+        return y
+    docs = _doclens(cu_doclens, B, L, x.device)
     st = lib().dd_rope(_ptr(x), _ptr(y), B, L, H, D, float(base), int(bool(inverse)),
                        _ptr(docs.dev) if docs else None, docs.n_docs if docs else 0,
                        int(bool(doc_positions)), _stream(x.device))
@@ -134,7 +146,7 @@ def forward_rope(q, k, v, base: float, causal: bool = True, cu_doclens=None,
     """Attention over rotated q and k.  Returns (o, lse, q_rot, k_rot); the
     rotated tensors are what ``backward_rope`` takes."""
     B, L = q.shape[0], q.shape[1]
-    docs = _doclens(cu_doclens, B, L, q.device)
+    docs = None if _empty(q) else _doclens(cu_doclens, B, L, q.device)
     qr = rope(q, base, docs, doc_positions)
     kr = rope(k, base, docs, doc_positions)
     o, lse = forward(qr, kr, v, causal, docs)
@@ -150,11 +162,13 @@ def backward_rope(q_rot, k_rot, v, o, lse, do, base: float, causal: bool = True,
     for t, n in ((k_rot, "k_rot"), (v, "v"), (o, "o"), (do, "do")):
         _check_tensor(t, n, q_rot.shape)
     _check_tensor(lse, "lse", (B, L, H), torch.float32)
+    dq, dk, dv = torch.empty_like(q_rot), torch.empty_like(q_rot), torch.empty_like(q_rot)
+    if _empty(q_rot):
+        return dq, dk, dv
     docs = _doclens(cu_doclens, B, L, q_rot.device)
     need = workspace_bytes(B, L, H, D)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q_rot.device)
-    dq, dk, dv = torch.empty_like(q_rot), torch.empty_like(q_rot), torch.empty_like(q_rot)
     st = lib().dd_attn_bwd_rope(_ptr(q_rot), _ptr(k_rot), _ptr(v), _ptr(o), _ptr(do), _ptr(lse),
                                 _ptr(dq), _ptr(dk), _ptr(dv), B, L, H, D, int(bool(causal)),
                                 _ptr(docs.dev) if docs else None, docs.n_docs if docs else 0,

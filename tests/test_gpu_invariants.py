@@ -144,6 +144,21 @@ def test_autograd_wrapper(cuda):
         assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("shape", [(0, 16, 2, 64), (2, 0, 2, 64), (2, 16, 0, 128)])
+def test_empty_inputs(cuda, shape):
+    # B, L or H = 0: empty results of the right shapes, no launch.
+    q, k, v, do = (torch.empty(shape, dtype=torch.bfloat16, device=cuda) for _ in range(4))
+    o, lse = dd.forward(q, k, v)
+    assert o.shape == shape and lse.shape == shape[:3] and lse.dtype == torch.float32
+    for g in dd.backward(q, k, v, o, lse, do):
+        assert g.shape == shape
+    assert dd.rope(q, 1e4).shape == shape
+    qg = q.clone().requires_grad_(True)
+    out = dd.attention(qg, k, v, rope_base=1e4)
+    out.backward(do)
+    assert out.shape == shape and qg.grad.shape == shape
+
+
 def test_errors_with_live_device(cuda):
     x = inputs(1, 64, 1, 64, 9, cuda)
     bad = torch.zeros(1, 64, 1, 80, dtype=torch.bfloat16, device=cuda)
