@@ -460,23 +460,21 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             // The A fragments are read in batches of KB_STEP k-steps before
-            // their products, so several LDS reads are in flight at once.
-            constexpr int KB_STEP = KK >= 8 ? 4 : KK;
-            // SEED: dP^T accumulates onto -delta (this lane's query), so the
+            // their products, so several LDS reads are in flight at once
+            // (two at D = 64, which keeps the kernel at 163 VGPRs, three
+            // waves per SIMD).
+            constexpr int KB_STEP = KK >= 8 ? 4 : 2;
+            // dP^T accumulates onto -delta (this lane's query), so the
             // products give dP - delta, and the fill runs beside the S
             // products instead of a subtraction after them.  The opaque copy
             // keeps the compiler from hoisting the filled registers out of
-            // the tile loop.  Not for the one-block D = 64 form: the earlier
-            // live range costs it a wave per SIMD (171 VGPRs).
-            constexpr bool SEED = D != 64 || PERSIST;
-            f32x16 s = f32x16{}, dp = f32x16{};
-            if constexpr (SEED) {
-                float nd = -my_delta;
-                asm volatile("" : "+v"(nd));
+            // the tile loop.
+            float nd = -my_delta;
+            asm volatile("" : "+v"(nd));
+            f32x16 s = f32x16{}, dp;
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    dp[r] = nd;
-            }
+            for (int r = 0; r < 16; ++r)
+                dp[r] = nd;
 #pragma unroll
             for (int k0 = 0; k0 < KK; k0 += KB_STEP) {
                 bf16x8 ka[KB_STEP], va[KB_STEP];
@@ -501,7 +499,7 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     const bool ok = (kr >= lo_r) & (kr <= hi_r);
                     p = ok ? p : 0.f;
                 }
-                dp[r] = SEED ? p * dp[r] : p * (dp[r] - my_delta);
+                dp[r] = p * dp[r];
             }
             bf16x8 kt[2][DB];
 #pragma unroll
