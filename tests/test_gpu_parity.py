@@ -58,6 +58,13 @@ def test_persistent_kernels_several_items_per_workgroup(cuda, D):
 
 
 @pytest.mark.parametrize("D", [64, 128])
+def test_persistent_kernels_non_causal(cuda, D):
+    # Without the causal mask every block spans its whole row.
+    B, bh = PERSIST_CASES[D]
+    check_case(B, 700, 3, D, causal=False, seed=13, bh=bh, tag=f"persistent D={D}, non-causal")
+
+
+@pytest.mark.parametrize("D", [64, 128])
 def test_persistent_kernels_document_masked(cuda, D):
     (B, bh), L, H = PERSIST_CASES[D], 700, 3
     lens = synth.lognormal_doc_lengths(2, total_tokens=B * L, median=300, sigma=0.8)
