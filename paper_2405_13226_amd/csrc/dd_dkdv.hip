@@ -423,20 +423,17 @@ hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s)
     const long long n_items = static_cast<long long>(nkb) * a.B * a.H;
     const long long all = (n_items + kXcds - 1) / kXcds * kXcds;
     hipStream_t st = static_cast<hipStream_t>(a.stream);
-    if (a.L > kPersistMaxSpan)
-        return launch_kernel(dkdv_kernel<128, false>, dim3(static_cast<unsigned>(all)),
-                             dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.ndelta, a.dK,
-                             a.dV, a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2,
-                             s.scale, nkb, s.rt, s.rope);
-    // Persistent: as many workgroups as are resident at once (one per CU).
-    const long long pgrid = persistent_grid<dkdv_kernel<128, true>>(64 * T::NW);
-    if (pgrid <= 0)
-        return hipErrorInvalidDevice;
-    const long long grid = std::min(pgrid, all);
-    return launch_kernel(dkdv_kernel<128, true>, dim3(static_cast<unsigned>(grid)),
-                         dim3(64 * T::NW), st, a.Q, a.K, a.V, a.dO, s.lse2, s.ndelta, a.dK, a.dV,
-                         a.B, a.L, a.H, a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale,
-                         nkb, s.rt, s.rope);
+    // Persistent for short rows, as many workgroups as are resident at once
+    // (one per CU); one item per workgroup otherwise, or when that many
+    // workgroups already cover every item.
+    const long long pgrid =
+        a.L <= kPersistMaxSpan ? persistent_grid<dkdv_kernel<128, true>>(64 * T::NW) : 0;
+    const bool persist = pgrid > 0 && pgrid < all;
+    return launch_kernel(persist ? dkdv_kernel<128, true> : dkdv_kernel<128, false>,
+                         dim3(static_cast<unsigned>(persist ? pgrid : all)), dim3(64 * T::NW), st,
+                         a.Q, a.K, a.V, a.dO, s.lse2, s.ndelta, a.dK, a.dV, a.B, a.L, a.H,
+                         a.causal ? 1 : 0, a.cu, a.n_docs, s.scale_log2, s.scale, nkb, s.rt,
+                         s.rope);
 }
 
 }  // namespace dd
