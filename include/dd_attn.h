@@ -35,10 +35,13 @@
  * Ownership.  Every tensor pointer is a DEVICE pointer owned by the caller,
  * including the backward workspace.  The library allocates no device memory
  * and keeps no pointer after a call returns.  Its only state is a per-device
- * cache of the compute-unit count (filled on first use, atomically) and the
- * opt-in timing records of dd_prof_enable(), so calls are thread-safe.  Work
- * is enqueued asynchronously on `stream` (a hipStream_t; NULL = the default
- * stream); outputs are valid once the caller synchronises.
+ * cache of the compute-unit count and a per-kernel cache of its occupancy
+ * (both filled on first use, atomically) and the opt-in timing records of
+ * dd_prof_enable(), so calls are thread-safe.  Work is enqueued
+ * asynchronously on `stream` (a hipStream_t; NULL = the default stream);
+ * outputs are valid once the caller synchronises.  A call enqueues kernel
+ * launches only (no allocation, memset or synchronisation), so it can be
+ * captured in a HIP graph and replayed.
  *
  * Errors.  Arguments are validated on the host before anything is enqueued;
  * on error nothing is launched and outputs are untouched.  No exception
