@@ -37,8 +37,8 @@ constexpr int kAhead = 4;
 //   role A (waves 0-3): K in registers; S = Q K^T, P = exp2(S*c - lse2)
 //                       (masked), P handed to role B through LDS,
 //                       dV^T += dO^T P;
-//   role B (waves 4-7): V in registers; dP - delta = dO V^T accumulated onto
-//   -delta, then dS = P (dP - delta),
+//   role B (waves 4-7): V in registers; dP - delta = dO V^T accumulated
+//                       onto -delta, dS = P (dP - delta),
 //                       dK^T += Q^T dS.
 // Each wave holds one accumulator set, so two waves fit per SIMD and one
 // wave's softmax arithmetic overlaps the other's matrix products.
