@@ -335,10 +335,9 @@ __device__ __forceinline__ QItem q_item(int bid, int nqb, int B, int L, int H, b
 
 // PERSIST = false: one query block per workgroup.  PERSIST = true (short
 // rows, D = 64 only; at D = 128 the item loop spills): a workgroup walks
-// its query blocks in the order of item_bid;
-// during a block's last key tile it DMAs the next block's first K/V tile
-// into the free stage, and right after that tile loads the next block's Q,
-// dO and O rows.
+// its query blocks in the order of item_bid; during a block's last key tile
+// it DMAs the next block's first K/V tile into the free stage, and right
+// after that tile loads the next block's Q, dO and O rows.
 template <int D, bool PERSIST>
 __global__ void __launch_bounds__(256, 2)
 dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
@@ -388,8 +387,8 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
     // Q, dO and O rows of this lane's query (k-slots 8g..8g+7 of each
     // 16-wide step; load_rows), then delta = rowsum(dO * O): a partial per
-    // lane, completed with the lane holding the other half of the row; with
-    // the LSE in log2 units both are written, in [B*H][L] rows, for the dK/dV
+    // lane, completed with the lane holding the other half of the row; -delta
+    // and the LSE in log2 units are written, in [B*H][L] rows, for the dK/dV
     // kernel that runs after this one (finish_rows).  A query past L reads
     // row L-1 instead (its probabilities are masked to exactly 0 by a select
     // and nothing of it is stored).
