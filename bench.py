@@ -26,9 +26,10 @@ Workloads (``--workload``):
 
 Prints ONE JSON line on stdout: the metric is useful attention TFLOP/s
 (forward 4*D and backward 10*D FLOPs per allowed (query, key) pair and head)
-over the whole bench step, with per-group times, tokens/s, the roofline of
-the dominant kernel (timed with HIP events on its own stream) and the fp64
-CPU oracle timed on a bounded sample of the same workload.
+over the whole bench step, with per-group times, tokens/s, per-length
+efficiency where lengths repeat (stream, curriculum), the roofline of the
+dominant kernel (timed with HIP events on its own stream) and the fp64 CPU
+oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -427,6 +428,23 @@ def main():
         "groups": per_group, "kernels": kern, "roofline": roofline,
         "sclk_mhz": sclk.summary(),
     }
+    # Streams repeat lengths: per-L efficiency over the steps of each length.
+    lens = [g["L"] for g in groups]
+    if len(set(lens)) < len(lens):
+        per_l = {}
+        for g, rec in zip(groups, per_group):
+            a = per_l.setdefault(g["L"], dict(steps=0, ms=0.0, flops=0.0, bytes=0.0))
+            a["steps"] += 1
+            a["ms"] += rec["ms"]
+            a["flops"] += g["flops_fwd"] + g["flops_bwd"]
+            a["bytes"] += sum(ddlib.dd.attention_bytes(g["B"], g["L"], H, D))
+        result["per_L"] = {
+            str(n): dict(steps=a["steps"], ms_mean=round(a["ms"] / a["steps"], 4),
+                         share_of_stream=round(a["ms"] / sum(r["ms"] for r in per_group), 4),
+                         tflops=round(a["flops"] / (a["ms"] * 1e-3) / 1e12, 2),
+                         mfma_frac=round(a["flops"] / (a["ms"] * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                         hbm_frac=round(a["bytes"] / (a["ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
+            for n, a in sorted(per_l.items())}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(groups, desc, args)
     print(json.dumps(result), flush=True)
