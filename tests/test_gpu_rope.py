@@ -167,3 +167,30 @@ def test_autograd_matches_functional(cuda):
     assert torch.equal(out.detach(), o)
     for a, b in zip((qa.grad, ka.grad, va.grad), g):
         assert torch.equal(a, b)
+
+
+def _rope_cases(n=12, seed=239):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        D = int(rng.choice([64, 128]))
+        L = int(rng.choice([int(rng.integers(1, 200)), int(rng.integers(200, 1500))]))
+        B, H = int(rng.integers(1, 30)), int(rng.integers(1, 7))
+        base = float(rng.choice([10000.0, 100000.0]))
+        cu, doc_pos = None, False
+        if rng.random() < 0.5 and B * L >= 2:
+            lens = synth.lognormal_doc_lengths(int(rng.integers(1 << 30)), total_tokens=B * L,
+                                               median=float(rng.choice([60, 300])), sigma=1.0)
+            cu = dd.chunk_doclens(lens, B * L)
+            doc_pos = bool(rng.random() < 0.5)
+        bh = sorted({(int(rng.integers(B)), int(rng.integers(H))) for _ in range(3)})
+        out.append((i, B, L, H, D, base, cu, doc_pos, bh))
+    return out
+
+
+@pytest.mark.parametrize("case", _rope_cases(), ids=lambda c: f"case{c[0]}")
+def test_attention_rope_random_configuration(cuda, case):
+    # Seeded random shapes, bases and document layouts (row or document-local
+    # positions), three sampled (b, h) slices each.
+    i, B, L, H, D, base, cu, doc_pos, bh = case
+    run_rope_attention(B, L, H, D, base, cu, doc_pos, seed=300 + i, bh=bh)
