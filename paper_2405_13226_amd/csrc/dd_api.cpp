@@ -37,6 +37,10 @@ int check_shape(int B, int L, int H, int D)
     long long rows = static_cast<long long>(B) * L * H;
     if (rows >= (1LL << 31))
         return DD_ERR_SHAPE;
+    // The kernels' LDS-DMA plans hold per-lane byte offsets of up to 256 token
+    // rows (row stride H * D elements) in 32 bits.
+    if (static_cast<long long>(H) * D >= (1LL << 23))
+        return DD_ERR_SHAPE;
     if (D != 64 && D != 128)
         return DD_ERR_HEADDIM;
     return DD_OK;

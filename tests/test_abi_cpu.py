@@ -95,6 +95,9 @@ def test_fwd_validation(lib):
     assert fwd(lib, L=0) == SHAPE
     assert fwd(lib, H=-1) == SHAPE
     assert fwd(lib, B=1 << 16, L=1 << 15, H=1) == SHAPE
+    # H * D >= 2^23 (the DMA plans' 32-bit row offsets), with B*L*H < 2^31
+    assert fwd(lib, B=1, L=1, H=1 << 16, D=128) == SHAPE
+    assert fwd(lib, B=1, L=1, H=1 << 17, D=64) == SHAPE
     assert fwd(lib, D=80) == HEADDIM
     assert fwd(lib, D=32) == HEADDIM
     assert fwd(lib, cu=fake(5), n_docs=0) == DOCLENS
