@@ -49,6 +49,9 @@ BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 METRIC = "attention fwd+bwd TFLOP/s and tokens/s per bucket at 65,536 tokens/step"
 BUCKETS = [256, 512, 1024, 2048, 4096, 8192]
+# D = 64 rows of at most this many tokens (without RoPE) run the one-kernel
+# backward.
+SHORT_MAX_ROW = 256
 
 
 def log(msg):
@@ -393,9 +396,17 @@ def main():
     for name, kid in _lib.KERNELS.items():
         ms, n = _lib.prof_read(kid)
         kern[name] = dict(total_ms=ms, launches=n, avg_ms=ms / n if n else 0.0)
-    per_pair = {"forward": 4, "backward_dkdv": 8, "backward_dq": 2}
-    alg = {name: sum(per_pair[name] * D * g["pairs"] for g in groups) * args.steps
-           for name in per_pair}
+    # Algorithmic FLOPs per (query, key) pair and head dim: the forward forms
+    # S and O (4); dK/dV forms S, dP, dV and dK (8); dQ forms dQ (2, its S and
+    # dP are recomputation); the one-kernel backward of D = 64 rows of at most
+    # 256 tokens without RoPE forms S, dP, dV, dK and dQ once (10).
+    def fused(g):
+        return D == 64 and g["L"] <= SHORT_MAX_ROW and not g.get("rope")
+
+    per_pair = {"forward": 4, "backward_dkdv": 8, "backward_dq": 2, "backward_short": 10}
+    alg = {name: sum(per_pair[name] * D * g["pairs"] for g in groups
+                     if name == "forward" or (name == "backward_short") == fused(g))
+           * args.steps for name in per_pair}
     # rope: each launch reads and writes one [tokens, H, D] bf16 tensor
     alg["rope"] = sum(2 * 2 * g["tokens"] * H * D * 2 for g in groups if g.get("rope")) \
         * args.steps
@@ -466,7 +477,7 @@ def run_layer(args, buckets, dev):
     gen.manual_seed(args.seed)
     x_all = torch.randn((TOKENS, d), generator=gen, device=dev).to(torch.bfloat16)
     dy_all = torch.randn((TOKENS, d), generator=gen, device=dev).to(torch.bfloat16)
-    attn_kernels = ("forward", "rope", "backward_dkdv", "backward_dq")
+    attn_kernels = ("forward", "rope", "backward_dkdv", "backward_dq", "backward_short")
     log(f"workload layer_1b: d={d} H={H} hidden={hidden} rope_base={ROPE_BASE:g}")
 
     def step(L):

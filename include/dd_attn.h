@@ -159,9 +159,9 @@ const char *dd_status_str(int status);
  * dd_prof_enable(0) stops recording and keeps the records.
  * dd_prof_read(kernel, &total_ms, &launches) waits for the recorded events
  * of that kernel and returns the sum of their elapsed times and the number of
- * launches; kernel ids are 0 forward, 2 backward dK/dV, 3 backward dQ (which
- * also forms delta and the log2 LSE), 4 rotary embedding; id 1 is reserved and
- * records nothing.  Returns
+ * launches; kernel ids are 0 forward, 1 the one-kernel backward of D = 64
+ * rows of at most 256 tokens without RoPE, 2 backward dK/dV, 3 backward dQ
+ * (which also forms delta and the log2 LSE), 4 rotary embedding.  Returns
  * DD_OK, DD_ERR_NULL for a NULL output pointer, DD_ERR_SHAPE for an unknown
  * kernel id, or DD_ERR_HIP if the runtime fails.  These calls are serialised
  * internally.

@@ -29,7 +29,7 @@ SIGNATURES = {
     "dd_prof_kernel_name": (ctypes.c_char_p, [_I]),
 }
 
-KERNELS = {"forward": 0, "backward_dkdv": 2, "backward_dq": 3, "rope": 4}  # id 1 reserved
+KERNELS = {"forward": 0, "backward_short": 1, "backward_dkdv": 2, "backward_dq": 3, "rope": 4}
 
 
 def prof_enable(on: bool) -> None:

@@ -21,7 +21,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdd_attn.so")
 
 ARCH = "gfx950"
-HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_dkdv.hip", "dd_prof.hip", "dd_rope.hip"]
+HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_dkdv.hip", "dd_bwd_short.hip", "dd_prof.hip", "dd_rope.hip"]
 # Extra flags per source.  The D = 128 dK/dV kernel is scheduled for
 # instruction-level parallelism (measured ~6% faster at L = 8192, neutral at
 # L = 256); the default strategy is faster for every other kernel.

@@ -657,8 +657,15 @@ static int launch_bwd_d(const BwdArgs &a)
     s.rope = a.rope_base > 0.0 ? (a.rope_doc && a.cu ? 2 : 1) : 0;
     s.rt = s.rope ? rope_epi(a.rope_base, D) : RopeEpi{};
 
-    // dQ first: it also writes -delta and log2-LSE, which dK/dV reads.
     hipError_t e;
+    if constexpr (D == 64)
+        if (a.L <= kShortMaxRow && s.rope == 0) {
+            ProfScope prof(K_BWD_SHORT, st);
+            e = launch_bwd_short(a, s);
+            return e == hipSuccess ? DD_OK : DD_ERR_HIP;
+        }
+
+    // dQ first: it also writes -delta and log2-LSE, which dK/dV reads.
     const int nqb = (a.L + QTile<D>::BM - 1) / QTile<D>::BM;
     {
         const long long all =

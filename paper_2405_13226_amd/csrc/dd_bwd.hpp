@@ -25,6 +25,11 @@ struct BwdScalars {
 // runtime's launch status.
 hipError_t launch_dkdv_paired(const BwdArgs &a, const BwdScalars &s);
 
+// Rows of at most this many tokens at D = 64 (without RoPE) take the one-kernel
+// backward of dd_bwd_short.hip: one workgroup per (b, h) slice.
+constexpr int kShortMaxRow = 256;
+hipError_t launch_bwd_short(const BwdArgs &a, const BwdScalars &s);
+
 // Rows of at most this many tokens take the persistent dK/dV forms: a key
 // block then visits few query tiles, and a workgroup that walks its blocks
 // back to back hides each block's set-up behind the previous one; longer

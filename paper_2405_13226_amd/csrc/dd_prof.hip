@@ -18,7 +18,7 @@ bool g_on = false;
 std::vector<Record> g_recs;  // records [0, g_used) are live; the rest are reusable
 size_t g_used = 0;
 
-const char *const kNames[K_COUNT] = {"forward", "reserved", "backward_dkdv", "backward_dq",
+const char *const kNames[K_COUNT] = {"forward", "backward_short", "backward_dkdv", "backward_dq",
                                      "rope"};
 
 }  // namespace

@@ -5,8 +5,9 @@
 
 namespace dd {
 
-// Id 1 is reserved (the backward's delta / log2-LSE pass runs inside dQ).
-enum KernelId { K_FWD = 0, K_RESERVED = 1, K_DKDV = 2, K_DQ = 3, K_ROPE = 4, K_COUNT = 5 };
+// The backward's delta / log2-LSE pass runs inside dQ (or inside the one-kernel
+// backward of short rows), so it has no id of its own.
+enum KernelId { K_FWD = 0, K_BWD_SHORT = 1, K_DKDV = 2, K_DQ = 3, K_ROPE = 4, K_COUNT = 5 };
 
 // Brackets one launch: records a start event on `stream` at construction and
 // a stop event at destruction, when timing is enabled (no-op otherwise).

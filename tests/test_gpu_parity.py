@@ -122,3 +122,20 @@ def test_longest_bucket_sampled(cuda):
     B, L, H, D = 4, 16384, 16, 128
     check_case(B, L, H, D, causal=True, seed=0, bh=[(3, 15)], tag="bucket L=16384 D=128")
     log("done")
+
+
+# D = 64 rows of at most 256 tokens (without RoPE) take the one-kernel
+# backward, with a row capacity of 64, 128 or 256 tokens; each capacity is
+# covered at and around its edges, with the causal mask, without it, and
+# with documents.
+@pytest.mark.parametrize("L", [1, 31, 64, 65, 100, 128, 129, 255, 256])
+@pytest.mark.parametrize("mode", ["causal", "full", "docs"])
+def test_short_rows_one_kernel_backward(cuda, L, mode):
+    B, H = 3, 2
+    cu = None
+    if mode == "docs":
+        lens = synth.lognormal_doc_lengths(L, total_tokens=B * L, median=max(L / 3, 1.0),
+                                           sigma=0.8)
+        cu = dd.chunk_doclens(lens, B * L)
+    check_case(B, L, H, 64, causal=mode != "full", cu=cu, seed=300 + L,
+               tag=f"one-kernel backward L={L} {mode}")
