@@ -23,6 +23,9 @@
 //             read them row-wise, dV^T and dK^T transposed (ds_read_b64_tr_b16).
 // Splitting dQ from dK/dV keeps every output owned by exactly one workgroup:
 // no atomics, deterministic results, at the cost of recomputing S and dP.
+// At D = 64, rows of at most 256 tokens without RoPE instead take one launch
+// (dd_bwd_short.hip) in which a slice fits one workgroup and S and dP are
+// formed once.
 #include "dd_bwd.hpp"
 #include "dd_tile.hpp"
 #include "dd_launch.hpp"

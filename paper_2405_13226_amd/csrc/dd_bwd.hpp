@@ -1,6 +1,7 @@
 // dd_bwd.hpp -- pieces of the attention backward shared by its translation
 // units (dd_bwd.hip: dK/dV for D = 64, dQ and the launcher;
-// dd_dkdv.hip: dK/dV for D = 128).
+// dd_dkdv.hip: dK/dV for D = 128; dd_bwd_short.hip: the one-kernel backward
+// of short rows at D = 64).
 #pragma once
 
 #include "dd_device.hpp"
