@@ -5,8 +5,9 @@ the caller's stream, so a forward + backward can be captured once and
 replayed.  Each replay is checked bit for bit against the eager result, with
 eager work of the program itself and a device synchronisation between the
 replays.  Rows of 700 tokens take the persistent kernels (several work items
-per workgroup); the document-masked case passes offsets prepared outside the
-capture (their host-to-device copy is not a graph operation).
+per workgroup), rows of 200 tokens at D=64 the one-kernel backward; the
+document-masked cases pass offsets prepared outside the capture (their
+host-to-device copy is not a graph operation).
 """
 import pytest
 import torch
@@ -20,12 +21,14 @@ from parity import log, to_dev
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("D,docs", [(64, False), (128, False), (64, True), (128, True)])
-def test_graph_replay_matches_eager(cuda, D, docs):
-    B, L, H = 2, 700, 2
+@pytest.mark.parametrize("D,docs,L", [(64, False, 700), (128, False, 700), (64, True, 700),
+                                      (128, True, 700), (64, False, 200), (64, True, 200)])
+def test_graph_replay_matches_eager(cuda, D, docs, L):
+    B, H = 2, 2
     x = {n: to_dev(a, cuda) for n, a in synth.attention_inputs(B, L, H, D, seed=40 + D).items()}
-    cu = DocLens([0, 150, 600, 700, 1100, 1400], B * L, cuda) if docs else None
-    log(f"graph case D={D} docs={docs}")
+    offs = [0, 150, 600, 700, 1100, 1400] if L == 700 else [0, 30, 170, 200, 290, 400]
+    cu = DocLens(offs, B * L, cuda) if docs else None
+    log(f"graph case D={D} docs={docs} L={L}")
 
     def step():
         o, lse = dd.forward(x["q"], x["k"], x["v"], cu_doclens=cu)
