@@ -187,3 +187,21 @@ def test_python_wrapper_checks_metadata_on_cpu():
         dd.rope(q, 10000.0)
     with pytest.raises(_lib.DDError):
         dd.DocLens([0, 3, 2, 4], 4, torch.device("cpu"))
+
+
+def test_kernel_ids_match_the_library(lib):
+    # The Python table of profiling ids names what the library reports for
+    # each id (a host-side lookup, no device call).
+    for name, kid in _lib.KERNELS.items():
+        assert lib.dd_prof_kernel_name(kid).decode() == name
+    assert lib.dd_prof_kernel_name(len(_lib.KERNELS)) is None
+    assert lib.dd_prof_kernel_name(-1) is None
+
+
+def test_bench_counts_the_one_kernel_backward_where_the_library_runs_it():
+    # bench.py's FLOP accounting assumes the one-kernel backward runs for
+    # D = 64 rows up to the library's limit (kShortMaxRow).
+    import bench
+    text = open(os.path.join(ROOT, "paper_2405_13226_amd", "csrc", "dd_bwd.hpp")).read()
+    m = re.search(r"constexpr int kShortMaxRow = (\d+);", text)
+    assert m and int(m.group(1)) == bench.SHORT_MAX_ROW
