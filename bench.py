@@ -59,19 +59,24 @@ def log(msg):
 
 
 def kernel_source_hash():
-    """sha256 of the HIP sources with comments and white space removed:
-    counter-based traffic is void once the code changes (comment edits leave
-    it valid)."""
+    """sha256 of the HIP sources and the build script, with comments and
+    white space removed: counter-based traffic is void once the code or its
+    compile flags change (comment edits leave it valid)."""
     import glob
     import hashlib
     import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2405_13226_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+    build = os.path.join(ROOT, "paper_2405_13226_amd", "build.py")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))) \
+            + [build]:
         with open(f, encoding="utf-8") as fh:
             code = fh.read()
-        code = re.sub(r"/\*.*?\*/", " ", code, flags=re.S)
-        code = re.sub(r"//[^\n]*", " ", code)
+        if f == build:
+            code = re.sub(r"#[^\n]*", " ", code)
+        else:
+            code = re.sub(r"/\*.*?\*/", " ", code, flags=re.S)
+            code = re.sub(r"//[^\n]*", " ", code)
         code = " ".join(code.split())
         h.update(os.path.basename(f).encode() + b"\0" + code.encode())
     return h.hexdigest()[:16]

@@ -22,10 +22,13 @@ LIB = os.path.join(PKG, "libdd_attn.so")
 
 ARCH = "gfx950"
 HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_dkdv.hip", "dd_bwd_short.hip", "dd_prof.hip", "dd_rope.hip"]
-# Extra flags per source.  The D = 128 dK/dV kernel is scheduled for
-# instruction-level parallelism (measured ~6% faster at L = 8192, neutral at
-# L = 256); the default strategy is faster for every other kernel.
-HIP_SOURCE_FLAGS = {"dd_dkdv.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]}
+# Extra flags per source.  The D = 128 dK/dV kernel and the one-kernel
+# short-row backward are scheduled for instruction-level parallelism
+# (measured: dK/dV ~6% faster at L = 8192, neutral at L = 256; short-row
+# backward 11% faster at L = 64, 2% at L = 128 and 256); the default strategy
+# is faster for every other kernel.
+_ILP = ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]
+HIP_SOURCE_FLAGS = {"dd_dkdv.hip": _ILP, "dd_bwd_short.hip": _ILP}
 CXX_SOURCES = ["dd_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 VALU forms are disabled for all device code.
