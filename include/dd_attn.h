@@ -28,7 +28,9 @@
  * a document-masked [Bc, L] batch whose documents all have length l and the
  * DD bucket batch [Bc*L/l, l] are the same bytes.
  *
- * Supported: D in {64, 128}; any L >= 1; B, H >= 1; B*L*H < 2^31; H*D < 2^23.
+ * Supported: D in {64, 128}; any L >= 1; B, H >= 1; B*L*H < 2^31; H*D < 2^23;
+ * B*H*ceil(L/128) <= 2^23 - 8 (the kernels' largest grids then stay below
+ * the 2^32 work-items of one dispatch).
  * Arithmetic: bf16 inputs, fp32 accumulation (matrix cores), fp32 softmax
  * statistics; probabilities and dS are rounded to bf16 before their products.
  *
@@ -63,7 +65,9 @@ extern "C" {
 typedef enum {
     DD_OK = 0,
     DD_ERR_NULL = 1,      /* a required pointer is NULL                        */
-    DD_ERR_SHAPE = 2,     /* B, L or H < 1, B*L*H >= 2^31 or H*D >= 2^23       */
+    DD_ERR_SHAPE = 2,     /* B, L or H < 1, B*L*H >= 2^31, H*D >= 2^23,
+                             B*H*ceil(L/128) > 2^23 - 8, or a RoPE base that
+                             is not finite and > 0                            */
     DD_ERR_HEADDIM = 3,   /* D is not 64 or 128                                */
     DD_ERR_DOCLENS = 4,   /* cu_doclens / n_docs inconsistent, or bad contents */
     DD_ERR_WORKSPACE = 5, /* backward workspace missing or too small           */

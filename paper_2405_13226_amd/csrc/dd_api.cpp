@@ -13,6 +13,10 @@
 
 namespace {
 
+// Bound on B * H * ceil(L / 128): (2^23 - 8) workgroups of 512 work-items
+// stay below 2^32 work-items.
+constexpr long long kMaxBlocks = (1LL << 23) - 8;
+
 struct Range {
     uintptr_t lo, hi;  // [lo, hi)
 };
@@ -40,6 +44,11 @@ int check_shape(int B, int L, int H, int D)
     // The kernels' LDS-DMA plans hold per-lane byte offsets of up to 256 token
     // rows (row stride H * D elements) in 32 bits.
     if (static_cast<long long>(H) * D >= (1LL << 23))
+        return DD_ERR_SHAPE;
+    // The largest one-block-per-workgroup grids hold ceil(L/128) * B * H
+    // workgroups (rounded up to a multiple of 8) of at most 512 work-items,
+    // and a dispatch holds fewer than 2^32 work-items.
+    if (rows / L * ((L + 127) / 128) > kMaxBlocks)
         return DD_ERR_SHAPE;
     if (D != 64 && D != 128)
         return DD_ERR_HEADDIM;
@@ -89,7 +98,9 @@ const char *dd_status_str(int status)
     switch (status) {
     case DD_OK: return "ok";
     case DD_ERR_NULL: return "a required pointer is NULL";
-    case DD_ERR_SHAPE: return "invalid shape: need B, L, H >= 1 and B*L*H < 2^31";
+    case DD_ERR_SHAPE:
+        return "invalid shape: need B, L, H >= 1, B*L*H < 2^31, H*D < 2^23, "
+               "B*H*ceil(L/128) <= 2^23 - 8 and a RoPE base that is finite and > 0";
     case DD_ERR_HEADDIM: return "unsupported head dimension: D must be 64 or 128";
     case DD_ERR_DOCLENS: return "invalid cu_doclens / n_docs";
     case DD_ERR_WORKSPACE: return "backward workspace missing or too small";

@@ -3,11 +3,11 @@
 * ``TokenBuckets.from_documents`` -- Sec. 2.1: every tokenized document is cut
   into the adjacent pieces of its binary decomposition; piece lengths 2^i go
   to bucket D_i, so every token lands in exactly one bucket.
-* ``curriculum_steps`` -- Algorithm 1 (Appendix B.2): for each of ``c``
-  cycles, take a fresh non-overlapping random subset s_{i,j} of every bucket
-  holding n_i / c tokens; while some subset of the cycle is non-empty, draw a
-  bucket with probability proportional to its odds o_i among the non-empty
-  subsets and take b / 2^i of its sequences without replacement.  Every step
+* ``curriculum_steps`` -- Algorithm 1 (Appendix B.2): training runs in ``c``
+  cycles; each cycle uses a fresh, disjoint random subset of every bucket
+  holding n_i / c of its tokens, and each of its steps takes b / 2^i unused
+  sequences of one bucket, the bucket chosen with probability proportional
+  to its odds o_i among the buckets the cycle has not used up.  Every step
   therefore holds b tokens of one sequence length (Sec. 2.2, VSL).
 * ``ODDS`` -- the sampling odds of Table "curriculum" for D_8..D_13.
 
@@ -67,6 +67,26 @@ class Step:
     rows: np.ndarray  # indices into TokenBuckets.seqs[length]
 
 
+def _bucket_order(steps: dict, odds: dict, rng: np.random.Generator) -> list:
+    """Bucket length of every step of one cycle.
+
+    The sampling rule: each step goes to a bucket that still has steps left
+    in the cycle, chosen with probability proportional to its odds among
+    those buckets; a cycle ends when every bucket's steps are used.
+    """
+    left = {L: n for L, n in steps.items() if n > 0}
+    order = []
+    while left:
+        live = sorted(left)
+        w = np.array([float(odds[L]) for L in live])
+        L = live[int(rng.choice(len(live), p=w / w.sum()))]
+        order.append(L)
+        left[L] -= 1
+        if left[L] == 0:
+            del left[L]
+    return order
+
+
 def curriculum_steps(rows_per_bucket: dict, tokens_per_bucket: dict, odds: dict,
                      cycles: int, tokens_per_step: int, rng: np.random.Generator):
     """Yield the steps of Algorithm 1 in training order.
@@ -84,25 +104,24 @@ def curriculum_steps(rows_per_bucket: dict, tokens_per_bucket: dict, odds: dict,
         have = rows_per_bucket.get(L, 0) * L
         if need > have:
             raise ValueError(f"bucket {L} holds {have} tokens, {need} requested")
-    # s_{i,j}: non-overlapping random subsets, whole steps per cycle.
+    # A step of bucket L holds b / L sequences; a cycle uses n_L / c tokens of
+    # it, i.e. n_L / (c b) whole steps.
+    seqs_per_step = {L: tokens_per_step // L for L in lengths}
+    steps = {L: tokens_per_bucket[L] // (cycles * tokens_per_step) for L in lengths}
+    # The cycles' subsets of each bucket: disjoint, drawn uniformly at random
+    # (one permutation of the bucket cut into consecutive runs), each holding
+    # the sequences of that cycle's steps in the order they are consumed.
     subsets = {}
     for L in lengths:
-        per_step = tokens_per_step // L
-        steps_per_cycle = tokens_per_bucket[L] // (cycles * tokens_per_step)
         perm = rng.permutation(rows_per_bucket.get(L, 0))
-        take = steps_per_cycle * per_step
-        subsets[L] = [perm[j * take:(j + 1) * take] for j in range(cycles)]
+        size = steps[L] * seqs_per_step[L]
+        subsets[L] = [perm[j * size:(j + 1) * size] for j in range(cycles)]
     for j in range(cycles):
-        pos = {L: 0 for L in lengths}
-        while True:
-            live = [L for L in lengths if pos[L] < subsets[L][j].size]
-            if not live:
-                break
-            w = np.array([float(odds[L]) if L in live else 0.0 for L in lengths])
-            L = lengths[int(rng.choice(len(lengths), p=w / w.sum()))]
-            per_step = tokens_per_step // L
-            rows = subsets[L][j][pos[L]:pos[L] + per_step]
-            pos[L] += per_step
+        used = {L: 0 for L in lengths}
+        for L in _bucket_order(steps, odds, rng):
+            k = used[L]
+            used[L] += 1
+            rows = subsets[L][j][k * seqs_per_step[L]:(k + 1) * seqs_per_step[L]]
             yield Step(cycle=j, length=L, rows=rows)
 
 

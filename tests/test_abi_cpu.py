@@ -98,6 +98,15 @@ def test_fwd_validation(lib):
     # H * D >= 2^23 (the DMA plans' 32-bit row offsets), with B*L*H < 2^31
     assert fwd(lib, B=1, L=1, H=1 << 16, D=128) == SHAPE
     assert fwd(lib, B=1, L=1, H=1 << 17, D=64) == SHAPE
+    # B*H*ceil(L/128) > 2^23 - 8 (a one-block-per-workgroup grid of 512-item
+    # workgroups would reach 2^32 work-items), with B*L*H < 2^31
+    assert fwd(lib, B=(1 << 23) - 7, L=1, H=1) == SHAPE
+    assert fwd(lib, B=(1 << 22) - 3, L=200, H=1) == SHAPE
+    assert fwd(lib, B=1 << 20, L=1, H=16) == SHAPE
+    assert bwd(lib, B=(1 << 23) - 7, L=1, H=1) == SHAPE
+    assert rope_call(lib, B=(1 << 23) - 7, L=1, H=1) == SHAPE
+    msg = lib.dd_status_str(SHAPE).decode()
+    assert "2^31" in msg and "H*D < 2^23" in msg and "ceil(L/128)" in msg and "RoPE" in msg
     assert fwd(lib, D=80) == HEADDIM
     assert fwd(lib, D=32) == HEADDIM
     assert fwd(lib, cu=fake(5), n_docs=0) == DOCLENS

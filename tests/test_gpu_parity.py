@@ -100,10 +100,13 @@ def test_single_token_documents(cuda):
     check_case(B, L, H, D, cu=cu, seed=3)
 
 
-@pytest.mark.parametrize("L,D", [(256, 64), (1024, 64), (8192, 64), (256, 128), (2048, 128),
-                                 (8192, 128)])
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("L", [256, 512, 1024, 2048, 4096, 8192])
 def test_full_step_buckets_sampled(cuda, L, D):
-    # A 65,536-token step: B = 65536 / L sequences, H = 16.
+    # A 65,536-token step: B = 65536 / L sequences, H = 16, in the launch
+    # configuration the benchmark times (every bucket of both head-dim
+    # sweeps: persistent and one-block forms, the one-kernel short-row
+    # backward at D = 64, L = 256).
     B, H = 65536 // L, 16
     bh = [(0, 0), (B - 1, H - 1), (B // 2, 7)]
     check_case(B, L, H, D, causal=True, seed=0, bh=bh, tag=f"bucket L={L} D={D}")
@@ -116,6 +119,34 @@ def test_concat_chunk_step_sampled(cuda):
     cu = dd.chunk_doclens(lens, B * L)
     check_case(B, L, H, D, causal=True, cu=cu, seed=0, bh=[(0, 0), (5, 9), (7, 15)],
                tag="chunk 8x8192 masked")
+
+
+def test_packed_dd_step_real_shape(cuda):
+    # A whole DD step in one document-masked launch, at the shape the
+    # benchmark times: the binary pieces (256..8192 tokens) of a 65,536-token
+    # step of log-normal documents (seed 0) packed into one row, H = 16,
+    # D = 64.  Pieces never attend to each other, so each sampled piece of
+    # the packed outputs must equal the oracle run on that piece alone (a DD
+    # sequence of its length): the longest pieces, a middle one and the two
+    # shortest, on two heads.
+    H, D = 16, 64
+    packed = dd.pack_step(synth.lognormal_doc_lengths(0), min_len=256, max_len=8192)
+    cu, L = packed.cu_doclens, packed.tokens
+    log(f"packed DD step: {len(cu) - 1} pieces, {L} tokens")
+    assert len(cu) - 1 >= 50 and L > 50000
+    inputs = synth.attention_inputs(1, L, H, D, seed=0, with_grad=True)
+    out = gpu_run(inputs, True, cu, "cuda:0")
+    lens = np.diff(cu)
+    order = np.argsort(lens, kind="stable")
+    picks = sorted({int(order[-1]), int(order[-2]), int(order[len(order) // 2]),
+                    int(order[0]), int(order[1])})
+    for i in picks:
+        lo, hi = int(cu[i]), int(cu[i + 1])
+        piece = {n: x[:, lo:hi] for n, x in inputs.items()}
+        piece_out = {n: t[:, lo:hi] for n, t in out.items()}
+        res = compare(piece, piece_out, True, None, [(0, 0), (0, 11)],
+                      tag=f"packed piece {i}: tokens {lo}..{hi - 1} (length {hi - lo})")
+        assert_ok(res)
 
 
 def test_longest_bucket_sampled(cuda):
