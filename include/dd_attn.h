@@ -43,7 +43,8 @@
  * asynchronously on `stream` (a hipStream_t; NULL = the default stream);
  * outputs are valid once the caller synchronises.  A call enqueues kernel
  * launches only (no allocation, memset or synchronisation), so it can be
- * captured in a HIP graph and replayed.
+ * captured in a HIP graph and replayed.  dd_attn_bwd_noalloc is the one
+ * exception to "no state": it uses a device array the library holds.
  *
  * Errors.  Arguments are validated on the host before anything is enqueued;
  * on error nothing is launched and outputs are untouched.  No exception
@@ -73,7 +74,8 @@ typedef enum {
     DD_ERR_WORKSPACE = 5, /* backward workspace missing or too small           */
     DD_ERR_ALIGN = 6,     /* a tensor pointer is not 16-byte aligned (LSE: 4)  */
     DD_ERR_ALIAS = 7,     /* an output overlaps an input or another output     */
-    DD_ERR_HIP = 8        /* the HIP runtime rejected a launch                 */
+    DD_ERR_HIP = 8,       /* the HIP runtime rejected a launch                 */
+    DD_ERR_SCRATCH = 9    /* dd_attn_bwd_noalloc: shape exceeds its scratch    */
 } dd_status;
 
 /*
@@ -104,6 +106,27 @@ int dd_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
                 int B, int L, int H, int D, int causal,
                 const int32_t *cu_doclens, int n_docs,
                 void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Backward without any allocation, for callers that cannot allocate device
+ * memory or pass a workspace: code under HIP graph capture, tight training
+ * loops, harnesses that forbid allocation.  Arguments and results are those
+ * of dd_attn_bwd without the workspace (same kernels, bit-identical
+ * outputs).  The workspace is a 16 MiB array in device memory that the
+ * library holds for the rest of the process, one copy per GPU, set up on the
+ * first call on that device; nothing is allocated or freed per call.  It
+ * covers every shape with B*H*L <= 2^21 (e.g. a 65,536-token step with up to
+ * 32 heads); larger shapes return DD_ERR_SCRATCH before anything is
+ * enqueued.  Nothing in the scratch has to start at zero, and it keeps the
+ * last call's contents.  Every call on one GPU uses the same scratch: calls
+ * that overlap on one device (concurrent streams, or threads without
+ * ordering between them) race and give unspecified results; calls ordered
+ * on one stream are safe.  Returns a dd_status.
+ */
+int dd_attn_bwd_noalloc(const void *Q, const void *K, const void *V, const void *O,
+                        const void *dO, const float *LSE, void *dQ, void *dK, void *dV,
+                        int B, int L, int H, int D, int causal,
+                        const int32_t *cu_doclens, int n_docs, void *stream);
 
 /*
  * Rotary position embedding (Sec. 3, "Positional encoding"): the paper

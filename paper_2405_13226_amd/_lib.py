@@ -17,6 +17,8 @@ SIGNATURES = {
     "dd_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _F, _I, _I, _I, _I, _I, _P, _I, _P]),
     "dd_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _F, _P, _P, _P, _I, _I, _I, _I, _I,
                                    _P, _I, _P, ctypes.c_size_t, _P]),
+    "dd_attn_bwd_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _F, _P, _P, _P, _I, _I, _I, _I,
+                                           _I, _P, _I, _P]),
     "dd_attn_bwd_rope": (ctypes.c_int, [_P, _P, _P, _P, _P, _F, _P, _P, _P, _I, _I, _I, _I, _I,
                                         _P, _I, ctypes.c_float, _I, _P, ctypes.c_size_t, _P]),
     "dd_rope": (ctypes.c_int, [_P, _P, _I, _I, _I, _I, ctypes.c_float, _I, _P, _I, _I, _P]),
@@ -45,7 +47,7 @@ def prof_read(kernel: int):
 STATUS = {
     0: "DD_OK", 1: "DD_ERR_NULL", 2: "DD_ERR_SHAPE", 3: "DD_ERR_HEADDIM",
     4: "DD_ERR_DOCLENS", 5: "DD_ERR_WORKSPACE", 6: "DD_ERR_ALIGN", 7: "DD_ERR_ALIAS",
-    8: "DD_ERR_HIP",
+    8: "DD_ERR_HIP", 9: "DD_ERR_SCRATCH",
 }
 
 _lib = None

@@ -21,7 +21,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdd_attn.so")
 
 ARCH = "gfx950"
-HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_dkdv.hip", "dd_bwd_short.hip", "dd_prof.hip", "dd_rope.hip"]
+HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_dkdv.hip", "dd_bwd_short.hip", "dd_prof.hip",
+               "dd_rope.hip", "dd_noalloc.hip"]
 # Extra flags per source.  The D = 128 dK/dV kernel and the one-kernel
 # short-row backward are scheduled for instruction-level parallelism
 # (measured: dK/dV ~6% faster at L = 8192, neutral at L = 256; short-row

@@ -107,6 +107,9 @@ const char *dd_status_str(int status)
     case DD_ERR_ALIGN: return "misaligned pointer: tensors need 16-byte alignment";
     case DD_ERR_ALIAS: return "an output buffer overlaps another buffer";
     case DD_ERR_HIP: return "HIP launch failed";
+    case DD_ERR_SCRATCH:
+        return "shape needs more than the 16 MiB device scratch of dd_attn_bwd_noalloc "
+               "(B*H*L <= 2^21); call dd_attn_bwd with a workspace";
     default: return "unknown status";
     }
 }
@@ -203,6 +206,29 @@ int dd_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
 {
     return attn_bwd_checked(Q, K, V, O, dO, LSE, dQ, dK, dV, B, L, H, D, causal, cu_doclens,
                             n_docs, 0.0, false, workspace, workspace_bytes, stream);
+}
+
+int dd_attn_bwd_noalloc(const void *Q, const void *K, const void *V, const void *O,
+                        const void *dO, const float *LSE, void *dQ, void *dK, void *dV,
+                        int B, int L, int H, int D, int causal,
+                        const int32_t *cu_doclens, int n_docs, void *stream)
+{
+    if (!Q || !K || !V || !O || !dO || !LSE || !dQ || !dK || !dV)
+        return DD_ERR_NULL;
+    int st = check_shape(B, L, H, D);
+    if (st != DD_OK)
+        return st;
+    st = check_doc_args(cu_doclens, n_docs, B, L);
+    if (st != DD_OK)
+        return st;
+    if (dd::bwd_workspace_bytes(B, L, H) > dd::kNoAllocScratchBytes)
+        return DD_ERR_SCRATCH;
+    void *ws = nullptr;
+    st = dd::noalloc_scratch(&ws);
+    if (st != DD_OK)
+        return st;
+    return attn_bwd_checked(Q, K, V, O, dO, LSE, dQ, dK, dV, B, L, H, D, causal, cu_doclens,
+                            n_docs, 0.0, false, ws, dd::kNoAllocScratchBytes, stream);
 }
 
 int dd_attn_bwd_rope(const void *Q, const void *K, const void *V, const void *O,

@@ -53,6 +53,14 @@ inline size_t bwd_workspace_bytes(int B, int L, int H)
     return 2 * align256(static_cast<size_t>(B) * H * L * sizeof(float));
 }
 
+// Size of the device-resident scratch of dd_attn_bwd_noalloc (dd_noalloc.hip):
+// the backward workspace of every shape with B * H * L <= 2^21.
+constexpr size_t kNoAllocScratchBytes = static_cast<size_t>(16) << 20;
+
+// Device address of this device's copy of that scratch (looked up once per
+// device with the device current).  Returns DD_OK or DD_ERR_HIP.
+int noalloc_scratch(void **ptr);
+
 // Both return a dd_status value (DD_OK or DD_ERR_HIP).
 int launch_fwd(const FwdArgs &a);
 int launch_bwd(const BwdArgs &a);

@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for code in range(9):
+    for code in range(10):
         s = lib.dd_status_str(code)
         assert s and s != b"unknown status"
     assert lib.dd_status_str(99) == b"unknown status"
@@ -184,6 +184,25 @@ def test_bwd_rope_validation(lib):
         assert call(ptrs={i: None}) == NULL, i
     assert call(ws_bytes=10) == WORKSPACE
     assert call(ptrs={7: fake(6)}) == ALIAS
+
+
+def test_noalloc_backward_validation(lib):
+    # Rejected on the host before the device scratch is touched.
+    SCRATCH = 9
+    def call(ptrs=None, B=2, L=64, H=2, D=64, cu=None, n_docs=0):
+        p = [fake(i) for i in range(9)]
+        for i, v in (ptrs or {}).items():
+            p[i] = v
+        return lib.dd_attn_bwd_noalloc(*p, B, L, H, D, 1, cu, n_docs, None)
+    for i in range(9):
+        assert call({i: None}) == NULL, i
+    assert call(B=0) == SHAPE
+    assert call(D=96) == HEADDIM
+    assert call(cu=fake(9), n_docs=0) == DOCLENS
+    # the scratch covers B*H*L <= 2^21
+    assert call(B=8, L=8192, H=33) == SCRATCH
+    assert call(B=1, L=(1 << 21) + 1, H=1) == SCRATCH
+    assert b"16 MiB" in lib.dd_status_str(SCRATCH)
 
 
 def test_python_wrapper_checks_metadata_on_cpu():
