@@ -26,10 +26,22 @@ Workloads (``--workload``):
 
 Prints ONE JSON line on stdout: the metric is useful attention TFLOP/s
 (forward 4*D and backward 10*D FLOPs per allowed (query, key) pair and head)
-over the whole bench step, with per-group times, tokens/s, per-length
-efficiency where lengths repeat (stream, curriculum), the roofline of the
-dominant kernel (timed with HIP events on its own stream) and the fp64 CPU
-oracle timed on a bounded sample of the same workload.
+over the whole bench step, with per-group times, tokens/s and per-kernel
+launch times, per-length efficiency where lengths repeat (stream,
+curriculum), the roofline of the dominant kernel launch (the kernel and
+group with the largest total time in the timed region, timed with HIP events
+on the kernel's own stream) and the fp64 CPU oracle timed on a bounded
+sample of every group of the workload.
+
+The default run (dd_sweep_d64 over every bucket) also times, after its own
+timed region, the D = 128 sweep and the concat-and-chunk vs DD comparison
+(``extra_workloads``; ``--no-extras`` skips them), and reports the L = 8192
+buckets of both sweeps in ``roofline.bucket_8192``.
+
+``--traffic-summary FETCH_DIR WRITE_DIR`` instead turns two rocprofv3 counter
+runs of this script (``--pmc FETCH_SIZE``, then ``--pmc WRITE_SIZE``, each
+with ``--copy-calibration``) into the HBM traffic per (kernel, group) that
+``profiles/traffic_<workload>.txt`` holds.
 """
 from __future__ import annotations
 
@@ -129,10 +141,10 @@ class SclkSampler:
         return dict(mean=round(sum(v) / len(v), 1), min=min(v), max=max(v), samples=len(v))
 
 
-def measured_traffic(workload, kernel):
-    """HBM bytes per launch of `kernel` from profiles/traffic_<workload>.txt
-    (key = value lines), or None if absent, for another kernel, or taken on
-    other kernel sources."""
+def measured_traffic(workload, kernel, group=None):
+    """HBM bytes per launch of `kernel` (in `group`, if given) from
+    profiles/traffic_<workload>.txt (key = value lines), or None if absent,
+    for another kernel or group, or taken on other kernel sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     if not os.path.exists(path):
         return None
@@ -144,7 +156,7 @@ def measured_traffic(workload, kernel):
                 kv[k.strip()] = v.strip()
     if kv.get("source_hash") != kernel_source_hash():
         return None
-    key = f"bytes_per_launch.{kernel}"
+    key = f"bytes_per_launch.{kernel}" + (f".{group}" if group else "")
     return int(float(kv[key])) if key in kv else None
 
 
@@ -168,6 +180,10 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before warmup, copy 1 GiB on the device 3 times (a kernel of known "
                          "traffic that scales FETCH_SIZE / WRITE_SIZE counter runs)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="default run only: skip the D=128 sweep and chunk_vs_dd extras")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 counter runs of this script (no GPU use)")
     return ap.parse_args()
 
 
@@ -249,32 +265,74 @@ def workload(name, seed, buckets=None):
 
 
 # ---------------------------------------------------------------------------
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): every (b, h) slice "
-              "of the attention path is independent, so there is no cross-GPU exchange to "
-              "measure; the figure is one MI355X's throughput.", file=sys.stderr)
-        sys.exit(2)
+# per-launch attribution
+# ---------------------------------------------------------------------------
+# Library kernel ids (dd_prof_kernel_name) and the algorithmic FLOPs per
+# allowed (query, key) pair, per head dim, of each: the forward forms S and
+# O (4); dK/dV forms S, dP, dV and dK (8); dQ forms dQ (2: its S and dP are
+# recomputation); the one-kernel backward of D = 64 rows of at most 256
+# tokens without RoPE forms S, dP, dV, dK and dQ once (10).
+PER_PAIR = {"forward": 4, "backward_dkdv": 8, "backward_dq": 2, "backward_short": 10}
 
+
+def split_by_group(launches, names, n_groups):
+    """[(kernel name, ms)] in launch order -> per group {kernel: [ms, ...]}.
+    Every group launches exactly one forward per step, preceded by its RoPE
+    launches (if any) and followed by its backward kernels."""
+    out = [dict() for _ in range(n_groups)]
+    gi = -1
+    for kid, ms in launches:
+        name = names[kid]
+        if name == "forward":
+            gi = (gi + 1) % n_groups
+            target = gi
+        elif name == "rope":
+            target = (gi + 1) % n_groups
+        else:
+            target = gi
+        out[target].setdefault(name, []).append(ms)
+    return out
+
+
+def kernel_alg(name, g):
+    """Algorithmic work of one launch of kernel `name` in group g: (amount,
+    'flop' or 'byte')."""
+    if name == "rope":  # reads and writes one [tokens, H, D] bf16 tensor
+        return 2 * g["tokens"] * g["H"] * g["D"] * 2, "byte"
+    return PER_PAIR[name] * g["D"] * g["pairs"], "flop"
+
+
+def roofline_of(name, g, avg_ms, workload):
+    amount, kind = kernel_alg(name, g)
+    if kind == "byte":
+        achieved = amount / (avg_ms * 1e-3) / 1e9
+        bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved = amount / (avg_ms * 1e-3) / 1e12
+        bound, peak, unit = "mfma", BF16_PEAK_TFLOPS, "TFLOP/s"
+    return dict(bound=bound, kernel=name, group=g["name"], achieved=round(achieved, 2), peak=peak,
+                unit=unit, frac=round(achieved / peak, 4),
+                traffic=measured_traffic(workload, name, g["name"]),
+                avg_ms=round(avg_ms, 5), algorithmic_per_launch=int(amount))
+
+
+# ---------------------------------------------------------------------------
+def run_workload(name, args, buckets, dev, seed):
+    """Warm up, time `args.steps` bench steps of workload `name` and return
+    the result dict (without cpu_baseline)."""
     import numpy as np
     import torch
     import paper_2405_13226_amd as ddlib
     from paper_2405_13226_amd import _lib
 
-    lib = ddlib.lib()  # raises if the HIP library is missing
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    buckets = [int(x) for x in args.buckets.split(",")] if args.buckets else None
-    if args.workload == "layer_1b":
-        return run_layer(args, buckets, dev)
-    groups, desc = workload(args.workload, args.seed, buckets)
+    lib = ddlib.lib()
+    groups, desc = workload(name, seed, buckets)
     H, D = desc["H"], desc["D"]
     ntok = max(g["tokens"] for g in groups)
 
     # Resident inputs (seeded N(0,1) bf16) and outputs, sized for the largest group.
     gen = torch.Generator(device=dev)
-    gen.manual_seed(args.seed)
+    gen.manual_seed(seed)
     shape = (ntok, H, D)
     q, k, v, do = (torch.randn(shape, generator=gen, device=dev, dtype=torch.float32)
                    .to(torch.bfloat16) for _ in range(4))
@@ -373,8 +431,13 @@ def main():
     tokens_step = sum(g["tokens"] for g in groups)
     value = flops_step / (ms_per_step * 1e-3) / 1e12
 
-    per_group = []
-    for g in groups:
+    # Every library launch of the timed region, attributed to its group.
+    names = {kid: n for n, kid in _lib.KERNELS.items()}
+    launches = _lib.prof_launches()
+    by_group = split_by_group(launches, names, len(groups))
+
+    per_group, pairs_ms = [], []
+    for g, kl in zip(groups, by_group):
         f = [e[0].elapsed_time(e[1]) for e in g["evs"]]
         b = [e[1].elapsed_time(e[2]) for e in g["evs"]]
         fm, bm = float(np.mean(f)), float(np.mean(b))
@@ -390,49 +453,32 @@ def main():
                    mfma_frac=round((g["flops_fwd"] + g["flops_bwd"]) / (tot * 1e-3) / 1e12
                                    / BF16_PEAK_TFLOPS, 4),
                    hbm_frac=round((fb + bb) / (tot * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
+        kern = {}
+        for kname, mss in kl.items():
+            avg = float(np.mean(mss))
+            r = roofline_of(kname, g, avg, desc["workload"])
+            kern[kname] = dict(launches=len(mss), avg_ms=round(avg, 5), achieved=r["achieved"],
+                               unit=r["unit"], frac=r["frac"])
+            pairs_ms.append((sum(mss), kname, g, avg))
+        rec["kernels"] = kern
         if "variant" in g:
             rec["variant"] = g["variant"]
         per_group.append(rec)
         log(f"  {g['name']:>16s}  fwd {fm:8.3f} ms  bwd {bm:8.3f} ms  "
-            f"{rec['tflops']:8.1f} TFLOP/s  {rec['tokens_per_s'] / 1e6:8.2f} Mtok/s")
+            f"{rec['tflops']:8.1f} TFLOP/s  {rec['tokens_per_s'] / 1e6:8.2f} Mtok/s  " +
+            " ".join(f"{k}={v['avg_ms']:.3f}ms/{v['frac']:.3f}" for k, v in kern.items()))
 
-    # Per-kernel durations from the library's event pairs (the kernel's stream).
-    kern = {}
-    for name, kid in _lib.KERNELS.items():
-        ms, n = _lib.prof_read(kid)
-        kern[name] = dict(total_ms=ms, launches=n, avg_ms=ms / n if n else 0.0)
-    # Algorithmic FLOPs per (query, key) pair and head dim: the forward forms
-    # S and O (4); dK/dV forms S, dP, dV and dK (8); dQ forms dQ (2, its S and
-    # dP are recomputation); the one-kernel backward of D = 64 rows of at most
-    # 256 tokens without RoPE forms S, dP, dV, dK and dQ once (10).
-    def fused(g):
-        return D == 64 and g["L"] <= SHORT_MAX_ROW and not g.get("rope")
-
-    per_pair = {"forward": 4, "backward_dkdv": 8, "backward_dq": 2, "backward_short": 10}
-    alg = {name: sum(per_pair[name] * D * g["pairs"] for g in groups
-                     if name == "forward" or (name == "backward_short") == fused(g))
-           * args.steps for name in per_pair}
-    # rope: each launch reads and writes one [tokens, H, D] bf16 tensor
-    alg["rope"] = sum(2 * 2 * g["tokens"] * H * D * 2 for g in groups if g.get("rope")) \
-        * args.steps
-    dom = max(kern, key=lambda n: kern[n]["total_ms"])
-    kd = kern[dom]
-    launches = max(kd["launches"], 1)
-    if dom == "rope":
-        achieved = alg[dom] / launches / (kd["avg_ms"] * 1e-3) / 1e9
-        roof = dict(bound="hbm", unit="GB/s", peak=HBM_PEAK_GBS)
-    else:
-        achieved = alg[dom] / launches / (kd["avg_ms"] * 1e-3) / 1e12
-        roof = dict(bound="mfma", unit="TFLOP/s", peak=BF16_PEAK_TFLOPS)
-    traffic = measured_traffic(desc["workload"], dom)
-    roofline = dict(bound=roof["bound"], kernel=dom, achieved=round(achieved, 2),
-                    peak=roof["peak"], unit=roof["unit"], frac=round(achieved / roof["peak"], 4),
-                    traffic=traffic, launches=kd["launches"], avg_ms=round(kd["avg_ms"], 5),
-                    algorithmic_per_launch=alg[dom] // launches)
-    for name in kern:
-        kern[name]["avg_ms"] = round(kern[name]["avg_ms"], 5)
-        kern[name]["total_ms"] = round(kern[name]["total_ms"], 3)
-    log(f"dominant kernel {dom}: {roofline}")
+    # Per-kernel totals over the whole timed region.
+    kern_all = {}
+    for kname in _lib.KERNELS:
+        mss = [m for kid, m in launches if names[kid] == kname]
+        kern_all[kname] = dict(total_ms=round(float(sum(mss)), 3), launches=len(mss),
+                               avg_ms=round(float(np.mean(mss)), 5) if mss else 0.0)
+    # Dominant kernel launch: the (kernel, group) with the largest total time.
+    _, dname, dg, davg = max(pairs_ms, key=lambda x: x[0])
+    roofline = roofline_of(dname, dg, davg, desc["workload"])
+    roofline["launches"] = len(by_group[groups.index(dg)][dname])
+    log(f"dominant kernel launch {dname} in {dg['name']}: {roofline}")
 
     result = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
@@ -441,7 +487,7 @@ def main():
         "data": "synthetic (seeded N(0,1) bf16 on device; log-normal document lengths)",
         "config": desc,
         "tokens_per_s": round(tokens_step / (ms_per_step * 1e-3)),
-        "groups": per_group, "kernels": kern, "roofline": roofline,
+        "groups": per_group, "kernels": kern_all, "roofline": roofline,
         "sclk_mhz": sclk.summary(),
     }
     # Streams repeat lengths: per-L efficiency over the steps of each length.
@@ -461,8 +507,80 @@ def main():
                          mfma_frac=round(a["flops"] / (a["ms"] * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
                          hbm_frac=round(a["bytes"] / (a["ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
             for n, a in sorted(per_l.items())}
+    del q, k, v, do, o, dq, dk, dv, qr, kr, lse, ws
+    torch.cuda.empty_cache()
+    return result, groups
+
+
+def bucket_summary(result, L=8192):
+    """Fwd+bwd fraction of the bf16 peak of the bucket of length L and the
+    roofline of its dominant kernel launch."""
+    for g in result["groups"]:
+        if g["L"] == L and g["B"] * g["L"] == TOKENS and "variant" not in g:
+            dom = max(g["kernels"].items(), key=lambda kv: kv[1]["avg_ms"] * kv[1]["launches"])
+            return dict(ms=g["ms"], fwd_ms=g["fwd_ms"], bwd_ms=g["bwd_ms"], tflops=g["tflops"],
+                        mfma_frac=g["mfma_frac"], dominant_kernel=dom[0],
+                        dominant_avg_ms=dom[1]["avg_ms"], dominant_frac=dom[1]["frac"])
+    return None
+
+
+def chunk_summary(result):
+    """Step times of the concat-and-chunk vs DD comparison (ms per variant)."""
+    g = result["groups"]
+    dd_ms = sum(r["ms"] for r in g if r.get("variant") == "dd")
+    pick = {r.get("variant"): r["ms"] for r in g if r.get("variant") in
+            ("dense", "masked", "dd_packed")}
+    return dict(dense_ms=pick.get("dense"), masked_ms=pick.get("masked"),
+                dd_per_bucket_ms=round(dd_ms, 4), dd_packed_ms=pick.get("dd_packed"),
+                dd_tokens_kept=result["config"]["dd_tokens_kept"], step_tokens=TOKENS)
+
+
+def main():
+    args = parse()
+    if args.traffic_summary:
+        return traffic_summary(args)
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): every (b, h) slice "
+              "of the attention path is independent, so there is no cross-GPU exchange to "
+              "measure; the figure is one MI355X's throughput.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2405_13226_amd as ddlib
+
+    ddlib.lib()  # raises if the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    buckets = [int(x) for x in args.buckets.split(",")] if args.buckets else None
+    if args.workload == "layer_1b":
+        return run_layer(args, buckets, dev)
+    result, groups = run_workload(args.workload, args, buckets, dev, args.seed)
+
+    extras = {}
+    if args.workload == "dd_sweep_d64" and buckets is None and not args.no_extras:
+        # Every target configuration in one run, after the headline's timed
+        # region: the D = 128 sweep and the concat-and-chunk vs DD step.
+        for name in ("dd_sweep_d128", "chunk_vs_dd"):
+            r, _ = run_workload(name, args, None, dev, args.seed)
+            keep = ("value", "unit", "ms_per_step", "tokens_per_s", "config", "roofline",
+                    "sclk_mhz", "groups")
+            extras[name] = {k: r[k] for k in keep}
+            if name == "chunk_vs_dd":
+                extras[name]["step_ms"] = chunk_summary(r)
+                log(f"chunk_vs_dd step ms: {extras[name]['step_ms']}")
+        result["extra_workloads"] = extras
+    b8 = {}
+    for key, r in (("d%d" % result["config"]["D"], result),
+                   ("d128", extras.get("dd_sweep_d128"))):
+        if r is not None and bucket_summary(r) is not None:
+            b8[key] = bucket_summary(r)
+    if b8:
+        result["roofline"]["bucket_8192"] = b8
+        log(f"L=8192 buckets: {b8}")
+    if "chunk_vs_dd" in extras:
+        result["chunk_vs_dd_step_ms"] = extras["chunk_vs_dd"]["step_ms"]
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(groups, desc, args)
+        result["cpu_baseline"] = cpu_baseline(groups, result, args)
     print(json.dumps(result), flush=True)
 
 
@@ -541,47 +659,163 @@ def run_layer(args, buckets, dev):
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(groups, desc, args):
-    """The fp64 oracle on a bounded sample: (b, h) pairs of one group."""
+def cpu_baseline(groups, result, args):
+    """The fp64 oracle timed on a bounded sample of every distinct group of
+    the workload: as many (b, h) pairs as the oracle has threads (all of
+    them, for smaller groups), on rows of the group's shape and document
+    layout, extrapolated to the whole group by its useful FLOPs (the
+    oracle's work per pair follows the allowed pairs).  Timing does not
+    depend on the values, so each sample draws only the rows it times."""
     import numpy as np
     import oracle
     import synth
+    from paper_2405_13226_amd import dd as ddh
 
-    # The middle group of the workload, its sampled (b, h) pairs.
-    g = groups[len(groups) // 2]
-    B, L, H, D = g["B"], g["L"], g["H"], g["D"]
-    rng = np.random.default_rng(args.seed)
-    per_pair_flops = (g["flops_fwd"] + g["flops_bwd"]) / (B * H)
-    x = {n: synth.normal_bf16((B, L, H, D), args.seed, i + 1) for i, n in enumerate("qkv")}
-    x["do"] = synth.normal_bf16((B, L, H, D), args.seed, 4)
+    cores = oracle.threads()
+    seen, per_group = {}, []
+    t_all = 0.0
+    for g, rec in zip(groups, result["groups"]):
+        B, L, H, D = g["B"], g["L"], g["H"], g["D"]
+        key = (B, L, H, D, g.get("rope"), None if g["cu"] is None else g["cu"].tobytes())
+        if key not in seen:
+            n = min(B * H, cores)
+            for _ in range(2):  # a second, larger sample if the first took < 0.5 s
+                Bs = -(-n // H)
+                pairs = [(b, h) for b in range(Bs) for h in range(H)][:n]
+                cu = None
+                if g["cu"] is not None:
+                    c = np.asarray(g["cu"], dtype=np.int64)
+                    c = c[c < Bs * L]
+                    cu = np.concatenate([c, [Bs * L]]).astype(np.int32)
+                x = {nm: synth.normal_bf16((Bs, L, H, D), args.seed, i + 1)
+                     for i, nm in enumerate(("q", "k", "v", "do"))}
+                t = time.perf_counter()
+                if g.get("rope"):
+                    from oracle import rope as orope
+                    orope.attn_fwd(x["q"], x["k"], x["v"], g["rope"], True, cu, bh=pairs)
+                    orope.attn_bwd(x["q"], x["k"], x["v"], x["do"], g["rope"], True, cu,
+                                   bh=pairs)
+                else:
+                    oracle.attn_fwd(x["q"], x["k"], x["v"], causal=True, cu_doclens=cu, bh=pairs)
+                    oracle.attn_bwd(x["q"], x["k"], x["v"], x["do"], causal=True,
+                                    cu_doclens=cu, bh=pairs)
+                secs = time.perf_counter() - t
+                t_all += secs
+                grow = min(B * H // n, int(np.ceil(0.5 / max(secs, 1e-3))))
+                if secs >= 0.5 or grow < 2:
+                    break
+                n *= grow
+            seg = ddh.segments(Bs, L, cu)
+            rows_pairs = int((seg * (seg + 1) // 2).sum())  # per head, over the Bs rows
+            sample_flops = 14 * D * rows_pairs * len(pairs) / H
+            rate = sample_flops / secs
+            seen[key] = dict(pairs_timed=len(pairs), seconds=round(secs, 3), rate=rate)
+            log(f"cpu oracle: {len(pairs)} (b,h) pairs of {g['name']} in {secs:.2f} s")
+        m = seen[key]
+        flops = g["flops_fwd"] + g["flops_bwd"]
+        ext = flops / m["rate"]
+        per_group.append(dict(name=g["name"], B=B, L=L, pairs_timed=m["pairs_timed"],
+                              pairs_total=B * H, seconds=m["seconds"],
+                              tflops=round(m["rate"] / 1e12, 6),
+                              extrapolated_seconds=round(ext, 2),
+                              tokens_per_s=round(g["tokens"] / ext, 1),
+                              gpu_ms=rec["ms"], gpu_speedup=round(ext / (rec["ms"] * 1e-3), 1)))
+    flops_step = sum(g["flops_fwd"] + g["flops_bwd"] for g in groups)
+    ext_step = sum(r["extrapolated_seconds"] for r in per_group)
+    return {"value": round(flops_step / ext_step / 1e12, 6), "unit": "TFLOP/s",
+            "cores": cores, "kind": "oracle",
+            "sample": f"fp64 fwd+bwd of up to {cores} (b, h) pairs of every distinct group "
+                      f"of {result['config']['workload']}, extrapolated by useful FLOPs to the "
+                      "whole step (per_group)",
+            "seconds": round(t_all, 2), "extrapolated_seconds_per_step": round(ext_step, 1),
+            "per_group": per_group}
 
-    def run(pairs):
-        t = time.perf_counter()
-        if g.get("rope"):
-            from oracle import rope as orope
-            orope.attn_fwd(x["q"], x["k"], x["v"], g["rope"], True, g["cu"], bh=pairs)
-            orope.attn_bwd(x["q"], x["k"], x["v"], x["do"], g["rope"], True, g["cu"], bh=pairs)
-        else:
-            oracle.attn_fwd(x["q"], x["k"], x["v"], causal=True, cu_doclens=g["cu"], bh=pairs)
-            oracle.attn_bwd(x["q"], x["k"], x["v"], x["do"], causal=True, cu_doclens=g["cu"],
-                            bh=pairs)
-        return time.perf_counter() - t
 
-    all_pairs = [(b, h) for b in range(B) for h in range(H)]
-    order = rng.permutation(len(all_pairs))
-    first = [all_pairs[order[0]]]
-    t1 = run(first)
-    n = int(min(len(all_pairs), max(1, args.cpu_seconds / max(t1, 1e-3))))
-    pairs = [all_pairs[i] for i in order[:n]]
-    secs = run(pairs) if n > 1 else t1
-    flops = per_pair_flops * n
-    log(f"cpu oracle: {n} (b,h) pairs of {g['name']} in {secs:.2f} s")
-    return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s",
-            "cores": oracle.threads(), "kind": "oracle",
-            "sample": f"{g['name']} (B={B}, L={L}, H={H}, D={D}): fwd+bwd of {n} of the "
-                      f"{B * H} (b, h) pairs, fp64",
-            "seconds": round(secs, 3),
-            "tokens_per_s": round(n * L / secs, 1)}
+def traffic_summary(args):
+    """profiles/traffic_<workload>.txt text (stdout) from two rocprofv3 counter
+    runs of this script: FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the
+    last bench step's library launches, per (kernel, group), scaled by what
+    the counters read for the 1 GiB copies of --copy-calibration."""
+    import csv
+    import glob
+    import re
+
+    import numpy as np
+
+    fam = {"fwd_kernel": "forward", "dq_kernel": "backward_dq", "dkdv1_kernel": "backward_dkdv",
+           "dkdv_kernel": "backward_dkdv", "bwd_short_kernel": "backward_short",
+           "rope_kernel": "rope"}
+
+    def read(d, counter):
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not f:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        disp = {}
+        for r in csv.DictReader(open(f[0])):
+            if r["Counter_Name"] != counter:
+                continue
+            did = int(r["Dispatch_Id"])
+            name = r["Kernel_Name"]
+            d0 = disp.setdefault(did, [name, 0.0])
+            d0[1] += float(r["Counter_Value"]) * 1024.0
+        return [disp[k] for k in sorted(disp)]
+
+    out = {}
+    for counter, d in (("FETCH_SIZE", args.traffic_summary[0]),
+                       ("WRITE_SIZE", args.traffic_summary[1])):
+        rows = read(d, counter)
+        # the three 1 GiB copies of --copy-calibration run right before the
+        # first library launch
+        first = next(i for i, (n, _) in enumerate(rows) if "dd::" in n)
+        copies = [v for n, v in rows[max(first - 3, 0):first] if "copy" in n.lower()]
+        if len(copies) != 3 or min(copies) < 2 ** 28:
+            raise SystemExit(f"{counter}: no copy-calibration dispatches before the first launch")
+        scale = float(2 ** 30) / float(np.median(copies))
+        lib_rows = []
+        for n, v in rows:
+            m = re.search(r"dd::(\w+)<", n)
+            if m and m.group(1) in fam:
+                lib_rows.append((fam[m.group(1)], v * scale))
+        out[counter] = (scale, lib_rows)
+    groups, desc = workload(args.workload, args.seed,
+                            [int(x) for x in args.buckets.split(",")] if args.buckets else None)
+    lines = [f"# HBM traffic per launch, workload {desc['workload']}, from rocprofv3 counter runs",
+             f"# command: rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) --output-format csv -d <dir> "
+             f"-o run -- python3 -u bench.py --workload {desc['workload']}"
+             + (f" --buckets {args.buckets}" if args.buckets else "") +
+             " --copy-calibration --steps 1 --warmup 1 --no-cpu-baseline --no-extras",
+             "# summary:  python3 bench.py --workload " + desc["workload"]
+             + (f" --buckets {args.buckets}" if args.buckets else "")
+             + " --traffic-summary <fetch dir> <write dir>",
+             "# FETCH_SIZE and WRITE_SIZE are KiB per dispatch; each is scaled by 2^30 / what it",
+             "# reads for a plain 1 GiB device copy (bytes of the last bench step's launches).",
+             f"workload = {desc['workload']}", f"source_hash = {kernel_source_hash()}",
+             f"fetch_scale = {out['FETCH_SIZE'][0]:.6f}", f"write_scale = {out['WRITE_SIZE'][0]:.6f}"]
+    for counter, key in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
+        lib_rows = out[counter][1]
+        names = [n for n, _ in lib_rows]
+        n_fwd = sum(1 for n in names if n == "forward")
+        if n_fwd % len(groups):
+            raise SystemExit("launch count does not match the workload's groups")
+        # index of the first launch of the last step: the (len(groups))-th
+        # forward from the end, with its preceding RoPE launches
+        fwd_idx = [i for i, n in enumerate(names) if n == "forward"]
+        start = fwd_idx[-len(groups)]
+        while start > 0 and names[start - 1] == "rope":
+            start -= 1
+        tail = lib_rows[start:]
+        kid = {"forward": 0, "rope": 4, "backward_dq": 3, "backward_dkdv": 2, "backward_short": 1}
+        nm = {v: k for k, v in kid.items()}
+        by = split_by_group([(kid[n], v) for n, v in tail], nm, len(groups))
+        for g, kl in zip(groups, by):
+            for kname, vals in kl.items():
+                out.setdefault("_bytes", {}).setdefault((kname, g["name"]), {})[key] = \
+                    float(np.mean(vals))
+    for (kname, gname), v in out["_bytes"].items():
+        lines.append(f"fetch_bytes_per_launch.{kname}.{gname} = {int(v['fetch'])}")
+        lines.append(f"write_bytes_per_launch.{kname}.{gname} = {int(v['write'])}")
+        lines.append(f"bytes_per_launch.{kname}.{gname} = {int(v['fetch'] + v['write'])}")
+    print("\n".join(lines))
 
 
 if __name__ == "__main__":

@@ -195,6 +195,14 @@ const char *dd_status_str(int status);
  */
 int dd_prof_enable(int on);
 int dd_prof_read(int kernel, double *total_ms, long long *launches);
+/*
+ * Every recorded launch in launch order: kernels[i] receives its kernel id
+ * and ms[i] its elapsed time, for the first min(capacity, recorded)
+ * launches since dd_prof_enable(1); *count receives the number recorded
+ * (kernels and ms may be NULL when capacity is 0).  Waits for the events it
+ * reads.  Returns DD_OK, DD_ERR_NULL or DD_ERR_HIP.
+ */
+int dd_prof_launches(int *kernels, double *ms, long long capacity, long long *count);
 const char *dd_prof_kernel_name(int kernel); /* NULL for an unknown id */
 
 #ifdef __cplusplus

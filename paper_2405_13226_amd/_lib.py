@@ -29,6 +29,8 @@ SIGNATURES = {
     "dd_prof_read": (ctypes.c_int, [_I, ctypes.POINTER(ctypes.c_double),
                                     ctypes.POINTER(ctypes.c_longlong)]),
     "dd_prof_kernel_name": (ctypes.c_char_p, [_I]),
+    "dd_prof_launches": (ctypes.c_int, [_P, _P, ctypes.c_longlong,
+                                        ctypes.POINTER(ctypes.c_longlong)]),
 }
 
 KERNELS = {"forward": 0, "backward_short": 1, "backward_dkdv": 2, "backward_dq": 3, "rope": 4}
@@ -43,6 +45,20 @@ def prof_read(kernel: int):
     ms, n = ctypes.c_double(0.0), ctypes.c_longlong(0)
     check(lib().dd_prof_read(int(kernel), ctypes.byref(ms), ctypes.byref(n)), "dd_prof_read")
     return ms.value, n.value
+
+def prof_launches():
+    """[(kernel id, ms)] of every launch recorded since prof_enable(True), in
+    launch order."""
+    import numpy as np
+    n = ctypes.c_longlong(0)
+    check(lib().dd_prof_launches(None, None, 0, ctypes.byref(n)), "dd_prof_launches")
+    kid = np.zeros(max(n.value, 1), dtype=np.int32)
+    ms = np.zeros(max(n.value, 1), dtype=np.float64)
+    check(lib().dd_prof_launches(kid.ctypes.data_as(ctypes.c_void_p),
+                                 ms.ctypes.data_as(ctypes.c_void_p), n.value, ctypes.byref(n)),
+          "dd_prof_launches")
+    return list(zip(kid[:n.value].tolist(), ms[:n.value].tolist()))
+
 
 STATUS = {
     0: "DD_OK", 1: "DD_ERR_NULL", 2: "DD_ERR_SHAPE", 3: "DD_ERR_HEADDIM",

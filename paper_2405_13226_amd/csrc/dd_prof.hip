@@ -87,6 +87,25 @@ int dd_prof_read(int kernel, double *total_ms, long long *launches)
     return DD_OK;
 }
 
+int dd_prof_launches(int *kernels, double *ms, long long capacity, long long *count)
+{
+    if (!count || (capacity > 0 && (!kernels || !ms)))
+        return DD_ERR_NULL;
+    std::lock_guard<std::mutex> lk(dd::g_mu);
+    const long long n = static_cast<long long>(dd::g_used);
+    for (long long i = 0; i < n && i < capacity; ++i) {
+        const dd::Record &r = dd::g_recs[static_cast<size_t>(i)];
+        float t = 0.f;
+        if (hipEventSynchronize(r.stop) != hipSuccess ||
+            hipEventElapsedTime(&t, r.start, r.stop) != hipSuccess)
+            return DD_ERR_HIP;
+        kernels[i] = r.kernel;
+        ms[i] = t;
+    }
+    *count = n;
+    return DD_OK;
+}
+
 const char *dd_prof_kernel_name(int kernel)
 {
     return (kernel >= 0 && kernel < dd::K_COUNT) ? dd::kNames[kernel] : nullptr;

@@ -217,6 +217,15 @@ def test_python_wrapper_checks_metadata_on_cpu():
         dd.DocLens([0, 3, 2, 4], 4, torch.device("cpu"))
 
 
+def test_prof_launches_without_records(lib):
+    # Nothing recorded: a count of 0, no device call.  A NULL count, or
+    # NULL arrays with a capacity, is rejected.
+    n = ctypes.c_longlong(-1)
+    assert lib.dd_prof_launches(None, None, 0, ctypes.byref(n)) == OK and n.value == 0
+    assert lib.dd_prof_launches(None, None, 0, None) == NULL
+    assert lib.dd_prof_launches(None, None, 4, ctypes.byref(n)) == NULL
+
+
 def test_kernel_ids_match_the_library(lib):
     # The Python table of profiling ids names what the library reports for
     # each id (a host-side lookup, no device call).

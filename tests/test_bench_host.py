@@ -1,0 +1,60 @@
+"""bench.py's host-side bookkeeping, on the CPU: attributing timed launches
+to the workload's groups, and turning counter runs into traffic per launch."""
+import csv
+import os
+import subprocess
+import sys
+
+import bench
+
+NAMES = {0: "forward", 1: "backward_short", 2: "backward_dkdv", 3: "backward_dq", 4: "rope"}
+
+
+def test_split_by_group_follows_launch_order():
+    # two steps of three groups: RoPE + forward + dQ + dK/dV, forward +
+    # one-kernel backward, forward + dQ + dK/dV
+    step = [(4, 0.1), (4, 0.1), (0, 1.0), (3, 2.0), (2, 3.0), (0, 4.0), (1, 5.0),
+            (0, 6.0), (3, 7.0), (2, 8.0)]
+    g = bench.split_by_group(step * 2, NAMES, 3)
+    assert g[0] == {"rope": [0.1] * 4, "forward": [1.0, 1.0], "backward_dq": [2.0, 2.0],
+                    "backward_dkdv": [3.0, 3.0]}
+    assert g[1] == {"forward": [4.0, 4.0], "backward_short": [5.0, 5.0]}
+    assert g[2] == {"forward": [6.0, 6.0], "backward_dq": [7.0, 7.0],
+                    "backward_dkdv": [8.0, 8.0]}
+
+
+def _write_counters(path, counter, rows):
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "run_counter_collection.csv"), "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for i, (name, kib) in enumerate(rows):
+            w.writerow([i + 1, name, counter, kib])
+
+
+def test_traffic_summary_scales_by_the_copy(tmp_path):
+    # --buckets 8192,4096 of the D=64 sweep: per step forward, dQ, dK/dV per
+    # group; one warm-up and one timed step.  The copies read half their
+    # bytes (FETCH) and write all of them (WRITE), as measured on gfx950.
+    def rows(per_kib, copy_kib):
+        r = [("void at::native::normal_kernel", 10.0)]
+        r += [("void at::native::copy_kernel", copy_kib)] * 3
+        for _ in range(2):
+            for base in (1000.0, 500.0):
+                r += [("void dd::fwd_kernel<64, false>(...)", base * per_kib),
+                      ("void dd::dq_kernel<64, false>(...)", 2 * base * per_kib),
+                      ("void dd::dkdv1_kernel<64, false>(...)", 3 * base * per_kib)]
+        return r
+    _write_counters(tmp_path / "f", "FETCH_SIZE", rows(1.0, 2 ** 19))
+    _write_counters(tmp_path / "w", "WRITE_SIZE", rows(0.5, 2 ** 20))
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--workload",
+                          "dd_sweep_d64", "--buckets", "8192,4096", "--traffic-summary",
+                          str(tmp_path / "f"), str(tmp_path / "w")],
+                         capture_output=True, text=True, check=True).stdout
+    kv = dict(l.split(" = ") for l in out.splitlines() if " = " in l and not l.startswith("#"))
+    assert float(kv["fetch_scale"]) == 2.0 and float(kv["write_scale"]) == 1.0
+    # dK/dV of the L=4096 group: 3 * 500 KiB read (x2), 3 * 250 KiB written
+    assert int(kv["fetch_bytes_per_launch.backward_dkdv.L=4096"]) == 3 * 500 * 1024 * 2
+    assert int(kv["write_bytes_per_launch.backward_dkdv.L=4096"]) == 3 * 250 * 1024
+    assert int(kv["bytes_per_launch.forward.L=8192"]) == 1000 * 1024 * 2 + 500 * 1024
