@@ -16,8 +16,11 @@ Workloads (``--workload``):
   curriculum     48 steps of the length curriculum of Algorithm 1 ("Grow-P2"
                  odds, 8 cycles, equal tokens from buckets 256 .. 8192), D = 128
   rope_d128      dd_sweep_d128 with rotary position embedding (base 100,000):
-                 q and k rotated before the forward, dq and dk rotated back in
-                 the backward kernels
+                 q and k rotated by dd_rope before the forward, dq and dk
+                 rotated back in the backward kernels
+  rope_d128_fused  the same, with q rotated inside the forward as it is
+                 loaded (dd_attn_fwd_rope, which also writes the rotated q
+                 for the backward); k still by dd_rope
   layer_1b       one OpenLM-1B block (d 2048, 16 heads, SwiGLU 5632, RoPE)
                  forward + backward per bucket L = 256 .. 8192 at 65,536
                  tokens: step time, attention's share of it, and the fit
@@ -167,7 +170,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dd_sweep_d64",
                     choices=["dd_sweep_d64", "dd_sweep_d128", "chunk_vs_dd", "stream",
-                             "curriculum", "rope_d128", "layer_1b", "tiny"])
+                             "curriculum", "rope_d128", "rope_d128_fused", "layer_1b", "tiny"])
     ap.add_argument("--buckets", default=None,
                     help="comma-separated subset of bucket lengths (sweeps only)")
     ap.add_argument("--seed", type=int, default=0)
@@ -201,17 +204,19 @@ def workload(name, seed, buckets=None):
         groups = [dict(name=f"L={L}", B=TOKENS // L, L=L, cu=None) for L in lens]
         desc = dict(workload=name, tokens_per_group=TOKENS, buckets=lens, H=H, D=D,
                     causal=True)
-    elif name == "rope_d128":
+    elif name in ("rope_d128", "rope_d128_fused"):
         # The D=128 sweep with rotary position embedding (base 100,000, the
         # paper's curriculum runs): the forward rotates q and k (two dd_rope
         # launches) before attention; the backward rotates dq and dk back in
         # its kernels' epilogues (dd_attn_bwd_rope).
         H, D = 16, 128
         lens = buckets or BUCKETS
-        groups = [dict(name=f"L={L}", B=TOKENS // L, L=L, cu=None, rope=ROPE_BASE)
-                  for L in lens]
+        fused = name.endswith("fused")
+        groups = [dict(name=f"L={L}", B=TOKENS // L, L=L, cu=None, rope=ROPE_BASE,
+                       rope_fused=fused) for L in lens]
         desc = dict(workload=name, tokens_per_group=TOKENS, buckets=lens, H=H, D=D,
-                    causal=True, rope_base=ROPE_BASE)
+                    causal=True, rope_base=ROPE_BASE,
+                    q_rotation="inside the forward" if fused else "dd_rope pass")
     elif name == "tiny":
         H, D = 4, 64
         groups = [dict(name="L=256", B=4, L=256, cu=None)]
@@ -357,13 +362,20 @@ def run_workload(name, args, buckets, dev, seed):
         cu = P(g["docs"].dev.data_ptr()) if g["docs"] else None
         nd = g["docs"].n_docs if g["docs"] else 0
         base = g.get("rope")
-        if base:
-            for src, dst in (("q", "qr"), ("k", "kr")):
-                st = lib.dd_rope(ptr[src], ptr[dst], B, L, H, D, base, 0, cu, nd, 0, sptr)
-                _lib.check(st, "dd_rope")
-        st = lib.dd_attn_fwd(ptr["qr"], ptr["kr"], ptr["v"], ptr["o"], ptr["lse"], B, L, H, D,
-                             1, cu, nd, sptr)
-        _lib.check(st, "dd_attn_fwd")
+        if base and g.get("rope_fused"):
+            st = lib.dd_rope(ptr["k"], ptr["kr"], B, L, H, D, base, 0, cu, nd, 0, sptr)
+            _lib.check(st, "dd_rope")
+            st = lib.dd_attn_fwd_rope(ptr["q"], ptr["kr"], ptr["v"], ptr["o"], ptr["lse"],
+                                      ptr["qr"], B, L, H, D, 1, cu, nd, base, 0, sptr)
+            _lib.check(st, "dd_attn_fwd_rope")
+        else:
+            if base:
+                for src, dst in (("q", "qr"), ("k", "kr")):
+                    st = lib.dd_rope(ptr[src], ptr[dst], B, L, H, D, base, 0, cu, nd, 0, sptr)
+                    _lib.check(st, "dd_rope")
+            st = lib.dd_attn_fwd(ptr["qr"], ptr["kr"], ptr["v"], ptr["o"], ptr["lse"], B, L, H,
+                                 D, 1, cu, nd, sptr)
+            _lib.check(st, "dd_attn_fwd")
         if mark:
             g["ev"][1].record(stream)
         if base:

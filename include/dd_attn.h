@@ -146,6 +146,23 @@ int dd_rope(const void *X, void *Y, int B, int L, int H, int D, float base, int 
             const int32_t *cu_doclens, int n_docs, int doc_positions, void *stream);
 
 /*
+ * Forward over rotated queries and keys with the query rotation done inside
+ * the attention kernel (Sec. 3, "Positional encoding"): Q holds the
+ * UNROTATED queries, K the keys already rotated by dd_rope (same base,
+ * cu_doclens and doc_positions).  Each query row is rotated as the kernel
+ * loads it into registers, bit-identically to dd_rope, and the forward of
+ * dd_attn_fwd runs over the rotated rows.  Q_rot (optional, NULL to skip):
+ * output [B, L, H, D] bf16 receiving the rotated queries, which is what
+ * dd_attn_bwd_rope takes; it must not overlap any other tensor.  Other
+ * arguments as for dd_attn_fwd and dd_rope.  Returns a dd_status
+ * (DD_ERR_SHAPE for a base that is not finite and > 0).
+ */
+int dd_attn_fwd_rope(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                     void *Q_rot, int B, int L, int H, int D, int causal,
+                     const int32_t *cu_doclens, int n_docs, float rope_base, int doc_positions,
+                     void *stream);
+
+/*
  * Backward for attention over rotated queries and keys.  Q and K are the
  * rotated tensors the forward consumed (dd_rope of the raw q and k with the
  * same base, cu_doclens and doc_positions); every other argument is as for

@@ -17,6 +17,8 @@ SIGNATURES = {
     "dd_attn_fwd": (ctypes.c_int, [_P, _P, _P, _P, _F, _I, _I, _I, _I, _I, _P, _I, _P]),
     "dd_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _F, _P, _P, _P, _I, _I, _I, _I, _I,
                                    _P, _I, _P, ctypes.c_size_t, _P]),
+    "dd_attn_fwd_rope": (ctypes.c_int, [_P, _P, _P, _P, _F, _P, _I, _I, _I, _I, _I, _P, _I,
+                                        ctypes.c_float, _I, _P]),
     "dd_attn_bwd_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _F, _P, _P, _P, _I, _I, _I, _I,
                                            _I, _P, _I, _P]),
     "dd_attn_bwd_rope": (ctypes.c_int, [_P, _P, _P, _P, _P, _F, _P, _P, _P, _I, _I, _I, _I, _I,

@@ -142,14 +142,31 @@ def rope(x, base: float, cu_doclens=None, doc_positions: bool = False, inverse: 
 
 
 def forward_rope(q, k, v, base: float, causal: bool = True, cu_doclens=None,
-                 doc_positions: bool = False):
+                 doc_positions: bool = False, fused: bool = True):
     """Attention over rotated q and k.  Returns (o, lse, q_rot, k_rot); the
-    rotated tensors are what ``backward_rope`` takes."""
+    rotated tensors are what ``backward_rope`` takes.  With ``fused`` the
+    attention kernel rotates q as it loads it (and writes q_rot); otherwise
+    q is rotated by a separate dd_rope pass.  k is always rotated by
+    dd_rope.  Both give bit-identical results."""
     B, L = q.shape[0], q.shape[1]
     docs = None if _empty(q) else _doclens(cu_doclens, B, L, q.device)
-    qr = rope(q, base, docs, doc_positions)
     kr = rope(k, base, docs, doc_positions)
-    o, lse = forward(qr, kr, v, causal, docs)
+    if not fused or _empty(q):
+        qr = rope(q, base, docs, doc_positions)
+        o, lse = forward(qr, kr, v, causal, docs)
+        return o, lse, qr, kr
+    _check_tensor(q, "q")
+    for t, n in ((kr, "k"), (v, "v")):
+        _check_tensor(t, n, q.shape)
+    H, D = q.shape[2], q.shape[3]
+    qr = torch.empty_like(q)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, L, H), dtype=torch.float32, device=q.device)
+    st = lib().dd_attn_fwd_rope(_ptr(q), _ptr(kr), _ptr(v), _ptr(o), _ptr(lse), _ptr(qr),
+                                B, L, H, D, int(bool(causal)),
+                                _ptr(docs.dev) if docs else None, docs.n_docs if docs else 0,
+                                float(base), int(bool(doc_positions)), _stream(q.device))
+    check(st, "dd_attn_fwd_rope")
     return o, lse, qr, kr
 
 

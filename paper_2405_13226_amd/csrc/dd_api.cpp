@@ -114,9 +114,11 @@ const char *dd_status_str(int status)
     }
 }
 
-int dd_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE,
-                int B, int L, int H, int D, int causal,
-                const int32_t *cu_doclens, int n_docs, void *stream)
+namespace {
+
+int attn_fwd_checked(const void *Q, const void *K, const void *V, void *O, float *LSE, void *Qrot,
+                     int B, int L, int H, int D, int causal, const int32_t *cu_doclens,
+                     int n_docs, double rope_base, bool rope_doc, void *stream)
 {
     if (!Q || !K || !V || !O || !LSE)
         return DD_ERR_NULL;
@@ -127,24 +129,50 @@ int dd_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE
     if (st != DD_OK)
         return st;
     if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
-        !aligned(LSE, 4))
+        !aligned(LSE, 4) || (Qrot && !aligned(Qrot, 16)))
         return DD_ERR_ALIGN;
     const size_t tb = static_cast<size_t>(B) * L * H * D * 2;
     const size_t lb = static_cast<size_t>(B) * L * H * 4;
     Range rq = range_of(Q, tb), rk = range_of(K, tb), rv = range_of(V, tb);
-    Range ro = range_of(O, tb), rl = range_of(LSE, lb);
+    Range ro = range_of(O, tb), rl = range_of(LSE, lb), rr = range_of(Qrot, Qrot ? tb : 0);
     for (Range in : {rq, rk, rv})
-        if (overlaps(ro, in) || overlaps(rl, in))
+        if (overlaps(ro, in) || overlaps(rl, in) || overlaps(rr, in))
             return DD_ERR_ALIAS;
-    if (overlaps(ro, rl))
+    if (overlaps(ro, rl) || overlaps(rr, ro) || overlaps(rr, rl))
         return DD_ERR_ALIAS;
     if (cu_doclens) {
         Range rc = range_of(cu_doclens, static_cast<size_t>(n_docs + 1) * 4);
-        if (overlaps(rc, ro) || overlaps(rc, rl))
+        if (overlaps(rc, ro) || overlaps(rc, rl) || overlaps(rc, rr))
             return DD_ERR_ALIAS;
     }
     dd::FwdArgs a{Q, K, V, O, LSE, B, L, H, D, causal != 0, cu_doclens, n_docs, stream};
+    a.rope_base = rope_base;
+    a.rope_doc = rope_doc;
+    a.Qrot = Qrot;
     return dd::launch_fwd(a);
+}
+
+bool valid_base(float base) { return std::isfinite(base) && base > 0.0f; }
+
+}  // namespace
+
+int dd_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                int B, int L, int H, int D, int causal,
+                const int32_t *cu_doclens, int n_docs, void *stream)
+{
+    return attn_fwd_checked(Q, K, V, O, LSE, nullptr, B, L, H, D, causal, cu_doclens, n_docs,
+                            0.0, false, stream);
+}
+
+int dd_attn_fwd_rope(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                     void *Q_rot, int B, int L, int H, int D, int causal,
+                     const int32_t *cu_doclens, int n_docs, float rope_base, int doc_positions,
+                     void *stream)
+{
+    if (!valid_base(rope_base))
+        return DD_ERR_SHAPE;
+    return attn_fwd_checked(Q, K, V, O, LSE, Q_rot, B, L, H, D, causal, cu_doclens, n_docs,
+                            static_cast<double>(rope_base), doc_positions != 0, stream);
 }
 
 namespace {
@@ -193,8 +221,6 @@ int attn_bwd_checked(const void *Q, const void *K, const void *V, const void *O,
     a.rope_doc = rope_doc;
     return dd::launch_bwd(a);
 }
-
-bool valid_base(float base) { return std::isfinite(base) && base > 0.0f; }
 
 }  // namespace
 

@@ -21,6 +21,7 @@
 #include "dd_internal.h"
 #include "dd_launch.hpp"
 #include "dd_prof.hpp"
+#include "dd_rope.hpp"
 #include "dd_attn.h"
 
 #include <algorithm>
@@ -78,12 +79,16 @@ __device__ __forceinline__ FwdItem fwd_item(int bid, int nqb, int B, int L, int 
 // rows): a workgroup walks its query blocks in the order of item_bid; during
 // a block's last key tile it DMAs the next block's first K/V tile into the
 // free stage, and after that tile loads the next block's Q rows.
-template <int D, bool PERSIST>
+// ROPE = true: Q holds the unrotated queries; each lane rotates its Q row
+// fragments right after loading them (positions and frequencies as
+// dd_rope, so the result is bit-identical to a dd_rope pass) and, when
+// Qrot is not null, writes the rotated rows there for the backward.
+template <int D, bool PERSIST, bool ROPE>
 __global__ void __launch_bounds__(256, 2)
 fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
            const uint16_t *__restrict__ V, uint16_t *__restrict__ O, float *__restrict__ LSE,
            int B, int L, int H, int causal_i, const int32_t *__restrict__ cu, int n_docs,
-           float scale_log2, int nqb)
+           float scale_log2, int nqb, uint16_t *__restrict__ Qrot, RopeEpi rt, int rope)
 {
     using T = FwdTile<D>;
     constexpr int KK = D / 16;  // k-steps of S^T
@@ -127,11 +132,41 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     // nothing of it is stored).
     bf16x8 qf8[KK];
     auto load_q = [&](const FwdItem &x) __attribute__((always_inline)) {
-        const int q = min(x.qb * T::BM + wave * 32 + l32, L - 1);
+        const int q_raw = x.qb * T::BM + wave * 32 + l32;
+        const int q = min(q_raw, L - 1);
         const uint16_t *src = Q + x.base + q * rs + g * 8;
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
             qf8[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(src + kk * 16));
+        if constexpr (ROPE) {
+            // Fragment kk holds dims kk*16 + 8g .. +7: pairs j = 8kk + 4g + e.
+            // The opaque copies keep the frequency arithmetic here, once
+            // per item, instead of hoisted across the tile loop.
+            int gl = g;
+            RopeEpi r = rt;
+            asm volatile("" : "+v"(gl), "+s"(r.p0), "+s"(r.p1), "+s"(r.p2), "+s"(r.p3),
+                         "+s"(r.r4), "+s"(r.r16));
+            const int pos = rope_position(x.b, L, q, cu, n_docs, rope);
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float sn, cs;
+                    rope_sincos(rope_theta_j(r, 8 * kk + 4 * gl + e), pos, sn, cs);
+                    float x0 = static_cast<float>(qf8[kk][2 * e]);
+                    float x1 = static_cast<float>(qf8[kk][2 * e + 1]);
+                    rope_pair<false>(x0, x1, sn, cs);
+                    qf8[kk][2 * e] = static_cast<__bf16>(x0);
+                    qf8[kk][2 * e + 1] = static_cast<__bf16>(x1);
+                }
+            }
+            if (Qrot != nullptr && q_raw < L) {
+                uint16_t *dst = Qrot + x.base + q * rs + g * 8;
+#pragma unroll
+                for (int kk = 0; kk < KK; ++kk)
+                    *reinterpret_cast<u32x4 *>(dst + kk * 16) = __builtin_bit_cast(u32x4, qf8[kk]);
+            }
+        }
     };
 
     // Per-lane LDS offsets (elements, relative to a tile).  K row reads: row
@@ -345,34 +380,44 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 #define DD_FWD_ARGS                                                                              \
     const uint16_t *__restrict__, const uint16_t *__restrict__, const uint16_t *__restrict__,   \
         uint16_t *__restrict__, float *__restrict__, int, int, int, int,                          \
-        const int32_t *__restrict__, int, float, int
-template __global__ void fwd_kernel<64, false>(DD_FWD_ARGS);
-template __global__ void fwd_kernel<64, true>(DD_FWD_ARGS);
-template __global__ void fwd_kernel<128, false>(DD_FWD_ARGS);
-template __global__ void fwd_kernel<128, true>(DD_FWD_ARGS);
+        const int32_t *__restrict__, int, float, int, uint16_t *__restrict__, RopeEpi, int
+template __global__ void fwd_kernel<64, false, false>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<64, true, false>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<128, false, false>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<128, true, false>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<64, false, true>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<64, true, true>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<128, false, true>(DD_FWD_ARGS);
+template __global__ void fwd_kernel<128, true, true>(DD_FWD_ARGS);
 #undef DD_FWD_ARGS
 
-template <int D>
+template <int D, bool ROPE>
 static int launch_fwd_d(const FwdArgs &a)
 {
     const int nqb = (a.L + FwdTile<D>::BM - 1) / FwdTile<D>::BM;
     const long long all = (static_cast<long long>(nqb) * a.B * a.H + kXcds - 1) / kXcds * kXcds;
     const float scale_log2 = kLog2e / sqrtf(static_cast<float>(D));
+    // RoPE: 0 off, 1 row positions, 2 document-local positions.
+    const int rope = ROPE ? (a.rope_doc && a.cu ? 2 : 1) : 0;
+    const RopeEpi rt = ROPE ? rope_epi(a.rope_base, D) : RopeEpi{};
     // Persistent for short rows: as many workgroups as are resident at once.
-    const long long pgrid = a.L <= kFwdPersistMaxSpan ? persistent_grid<fwd_kernel<D, true>>(256) : 0;
+    const long long pgrid =
+        a.L <= kFwdPersistMaxSpan ? persistent_grid<fwd_kernel<D, true, ROPE>>(256) : 0;
     const bool persist = pgrid > 0 && pgrid < all;
     ProfScope prof(K_FWD, static_cast<hipStream_t>(a.stream));
     const hipError_t e = launch_kernel(
-        persist ? fwd_kernel<D, true> : fwd_kernel<D, false>,
+        persist ? fwd_kernel<D, true, ROPE> : fwd_kernel<D, false, ROPE>,
         dim3(static_cast<unsigned>(persist ? pgrid : all)), dim3(256),
         static_cast<hipStream_t>(a.stream), a.Q, a.K, a.V, a.O, a.LSE, a.B, a.L, a.H,
-        a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, nqb);
+        a.causal ? 1 : 0, a.cu, a.n_docs, scale_log2, nqb, a.Qrot, rt, rope);
     return e == hipSuccess ? DD_OK : DD_ERR_HIP;
 }
 
 int launch_fwd(const FwdArgs &a)
 {
-    return a.D == 64 ? launch_fwd_d<64>(a) : launch_fwd_d<128>(a);
+    if (a.rope_base > 0.0)
+        return a.D == 64 ? launch_fwd_d<64, true>(a) : launch_fwd_d<128, true>(a);
+    return a.D == 64 ? launch_fwd_d<64, false>(a) : launch_fwd_d<128, false>(a);
 }
 
 }  // namespace dd

@@ -17,6 +17,9 @@ struct FwdArgs {
     const int32_t *cu;
     int n_docs;
     void *stream;
+    double rope_base = 0.0;  // > 0: Q is unrotated; rotate it at its load
+    bool rope_doc = false;   // document-local positions
+    void *Qrot = nullptr;    // optional output: the rotated Q
 };
 
 struct BwdArgs {

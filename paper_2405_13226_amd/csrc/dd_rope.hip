@@ -18,7 +18,7 @@ namespace dd {
 template <int D, bool INV>
 __global__ void __launch_bounds__(256)
 rope_kernel(const uint16_t *__restrict__ X, uint16_t *__restrict__ Y, int B, int L, int H,
-            RopeTheta rt, const int32_t *__restrict__ cu, int n_docs, int doc)
+            RopeEpi rt, const int32_t *__restrict__ cu, int n_docs, int doc)
 {
     constexpr int CG = D / 8;  // 8-dim chunks per row
     const long long total = static_cast<long long>(B) * L * H * CG;
@@ -40,7 +40,7 @@ rope_kernel(const uint16_t *__restrict__ X, uint16_t *__restrict__ Y, int B, int
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             float s, c;
-            rope_sincos(rt.th[cg * 4 + e], pos, s, c);
+            rope_sincos(rope_theta_j(rt, cg * 4 + e), pos, s, c);
             float x0 = static_cast<float>(x[2 * e]), x1 = static_cast<float>(x[2 * e + 1]);
             rope_pair<INV>(x0, x1, s, c);
             y[2 * e] = static_cast<__bf16>(x0);
@@ -51,21 +51,13 @@ rope_kernel(const uint16_t *__restrict__ X, uint16_t *__restrict__ Y, int B, int
 }
 
 #define DD_ROPE_ARGS                                                                             \
-    const uint16_t *__restrict__, uint16_t *__restrict__, int, int, int, RopeTheta,             \
+    const uint16_t *__restrict__, uint16_t *__restrict__, int, int, int, RopeEpi,               \
         const int32_t *__restrict__, int, int
 template __global__ void rope_kernel<64, false>(DD_ROPE_ARGS);
 template __global__ void rope_kernel<64, true>(DD_ROPE_ARGS);
 template __global__ void rope_kernel<128, false>(DD_ROPE_ARGS);
 template __global__ void rope_kernel<128, true>(DD_ROPE_ARGS);
 #undef DD_ROPE_ARGS
-
-RopeTheta rope_theta(double base, int D)
-{
-    RopeTheta rt{};
-    for (int j = 0; j < D / 2 && j < kMaxHalfD; ++j)
-        rt.th[j] = std::pow(base, -2.0 * j / D);
-    return rt;
-}
 
 RopeEpi rope_epi(double base, int D)
 {
@@ -85,7 +77,7 @@ static int launch_rope_d(const RopeArgs &a)
     hipStream_t st = static_cast<hipStream_t>(a.stream);
     ProfScope prof(K_ROPE, st);
     const hipError_t e = launch_kernel(rope_kernel<D, INV>, dim3(blocks), dim3(256), st, a.X, a.Y,
-                                       a.B, a.L, a.H, rope_theta(a.base, D), a.cu, a.n_docs,
+                                       a.B, a.L, a.H, rope_epi(a.base, D), a.cu, a.n_docs,
                                        a.doc ? 1 : 0);
     return e == hipSuccess ? DD_OK : DD_ERR_HIP;
 }

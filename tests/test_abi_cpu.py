@@ -186,6 +186,24 @@ def test_bwd_rope_validation(lib):
     assert call(ptrs={7: fake(6)}) == ALIAS
 
 
+def test_fused_rope_forward_validation(lib):
+    def call(ptrs=None, B=2, L=64, H=2, D=64, base=1e4, cu=None, n_docs=0):
+        p = [fake(i) for i in range(6)]
+        for i, v in (ptrs or {}).items():
+            p[i] = v
+        return lib.dd_attn_fwd_rope(*p[:5], p[5], B, L, H, D, 1, cu, n_docs, base, 0, None)
+    for i in range(5):
+        assert call({i: None}) == NULL, i
+    for base in (0.0, -1.0, float("nan"), float("inf")):
+        assert call(base=base) == SHAPE
+    assert call(B=0) == SHAPE
+    assert call(D=96) == HEADDIM
+    assert call({5: fake(5, 8)}) == ALIGN
+    assert call({5: fake(0, 64)}) == ALIAS      # Q_rot overlaps Q
+    assert call({5: fake(3, 64)}) == ALIAS      # Q_rot overlaps O
+    assert call({5: fake(4)}) == ALIAS          # Q_rot overlaps LSE
+
+
 def test_noalloc_backward_validation(lib):
     # Rejected on the host before the device scratch is touched.
     SCRATCH = 9

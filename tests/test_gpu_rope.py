@@ -5,9 +5,11 @@ through the C ABI against the fp64 oracle (oracle/rope.py).
   bf16, up to half a bf16 ulp plus the fp32 evaluation error of the rotation
   (angle reduced in double, fp32 sine/cosine: 2^-17 of the pair's magnitude);
   positions up to 16,383 exercise the angle reduction.
-* Attention over rotated q, k (dd_rope + dd_attn_fwd, dd_attn_bwd_rope):
-  the tolerances of tests/parity.py against the oracle with the rotated q, k
-  rounded to bf16 (its stated reading of the precision).
+* Attention over rotated q, k (dd_rope of k, dd_attn_fwd_rope rotating q
+  as it loads it, dd_attn_bwd_rope): the tolerances of tests/parity.py
+  against the oracle with the rotated q, k rounded to bf16 (its stated
+  reading of the precision); the fused query rotation is bit-identical to a
+  dd_rope pass followed by dd_attn_fwd.
 * The DD / masked-chunk equivalence with document-local positions.
 """
 import numpy as np
@@ -130,6 +132,33 @@ def test_attention_rope_persistent_dkdv(cuda, B, D):
 def test_attention_rope_full_bucket_sampled(cuda):
     B, L, H, D = 8, 8192, 16, 128
     run_rope_attention(B, L, H, D, 100000.0, seed=0, bh=[(0, 0), (7, 15), (3, 8)])
+
+
+@pytest.mark.parametrize("B,L,H,D,base,docs,doc_pos", [
+    (2, 300, 3, 64, 10000.0, False, False),     # persistent forward
+    (2, 300, 3, 128, 100000.0, True, True),
+    (48, 700, 3, 64, 100000.0, True, False),    # several items per workgroup
+    (1, 4100, 2, 64, 10000.0, False, False),    # one block per workgroup, ragged
+    (1, 16384, 1, 128, 10000.0, True, True),    # long positions
+    (3, 1000, 2, 128, 500000.0, False, False),
+])
+def test_fused_query_rotation_is_bit_identical(cuda, B, L, H, D, base, docs, doc_pos):
+    # The forward that rotates q as it loads it gives the same rotated q, O
+    # and LSE, bit for bit, as a dd_rope pass followed by dd_attn_fwd.
+    import paper_2405_13226_amd as pkg
+    log(f"fused rope forward B={B} L={L} H={H} D={D} base={base:g} docs={docs} doc_pos={doc_pos}")
+    inp = synth.attention_inputs(B, L, H, D, seed=L + D, with_grad=False)
+    q, k, v = (to_dev(inp[n], cuda_dev()) for n in ("q", "k", "v"))
+    cu = None
+    if docs:
+        lens = synth.lognormal_doc_lengths(L, total_tokens=B * L, median=200, sigma=1.0)
+        cu = dd.chunk_doclens(lens, B * L)
+    f = pkg.forward_rope(q, k, v, base, True, cu, doc_pos, fused=True)
+    u = pkg.forward_rope(q, k, v, base, True, cu, doc_pos, fused=False)
+    torch.cuda.synchronize()
+    for name, a, b in zip(("o", "lse", "q_rot", "k_rot"), f, u):
+        assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                           b.view(torch.int16) if b.dtype == torch.bfloat16 else b), name
 
 
 def test_rope_dd_equals_masked_chunk_with_document_positions(cuda):
