@@ -178,6 +178,66 @@ int dd_attn_bwd_rope(const void *Q, const void *K, const void *V, const void *O,
                      int doc_positions, void *workspace, size_t workspace_bytes,
                      void *stream);
 
+/*
+ * The rest of one transformer block of the paper's OpenLM models (Sec. 3.1;
+ * Appendix, Table "openlm1b": hidden dimension 2048, 16 heads, SwiGLU
+ * width 5632), so that a whole block step runs in this library: its
+ * projections and MLP products, its LayerNorms and the SwiGLU.  Same
+ * conventions as above: device pointers owned by the caller, host-side
+ * validation before anything is enqueued, asynchronous on `stream`, no
+ * allocation, a dd_status return.
+ *
+ * dd_gemm: C[M, N] = op(A) op(B) (+ R), bf16 inputs and outputs, fp32
+ * accumulation on the matrix cores, all matrices row-major with row strides
+ * (elements) lda, ldb, ldc.  op(A) = A stored [M][K], or (trans_a) A^T with
+ * A stored [K][M]; op(B) = B stored [K][N], or (trans_b) B^T with B stored
+ * [N][K]; trans_a and trans_b are not both set.  A forward projection
+ * y = x W is (x, W); its backward is dx = (dy, W^T) and dW = (x^T, dy).
+ * R: NULL, or a bf16 [M][N] matrix (row stride ldc) added to the rounded
+ * product before the final rounding (a residual connection); R may be C
+ * itself (in-place accumulation), otherwise it must not overlap C.
+ * M and N multiples of 256, K a multiple of 64 (DD_ERR_SHAPE otherwise);
+ * strides multiples of 8 and pointers 16-byte aligned (DD_ERR_ALIGN).  C
+ * must not overlap A or B.  workspace: fp32 scratch of
+ * dd_gemm_workspace_bytes(M, N, K) bytes for the split reduction of long-K
+ * products (the weight gradients); may be NULL when that is 0.
+ */
+int dd_gemm(const void *A, long long lda, int trans_a, const void *B, long long ldb, int trans_b,
+            const void *R, void *C, long long ldc, int M, int N, int K, void *workspace,
+            size_t workspace_bytes, void *stream);
+size_t dd_gemm_workspace_bytes(int M, int N, int K); /* 0: none needed, or invalid */
+
+/*
+ * LayerNorm over the rows of X [rows, d] (bf16, d in {512, 1024, 2048}):
+ * Y = (X - mean) / sqrt(var + eps) * w + b with the biased variance of the
+ * row; w, b: bf16 [d]; mean, rstd: fp32 [rows] outputs kept for the
+ * backward (rstd = 1 / sqrt(var + eps)).  eps finite and > 0.
+ */
+int dd_layernorm_fwd(const void *X, const void *w, const void *b, void *Y, float *mean,
+                     float *rstd, int rows, int d, float eps, void *stream);
+/*
+ * Its backward for upstream gradient dY [rows, d]: dX [rows, d] (plus dRes,
+ * an optional bf16 [rows, d] gradient added before rounding, e.g. the
+ * residual branch), and the parameter gradients dw, db (bf16 [d], summed
+ * over the rows).  workspace: fp32 scratch of
+ * dd_layernorm_bwd_workspace_bytes(rows, d) bytes.  Outputs must not
+ * overlap inputs or each other.
+ */
+int dd_layernorm_bwd(const void *X, const void *w, const float *mean, const float *rstd,
+                     const void *dY, const void *dRes, void *dX, void *dw, void *db, int rows,
+                     int d, void *workspace, size_t workspace_bytes, void *stream);
+size_t dd_layernorm_bwd_workspace_bytes(int rows, int d);
+
+/*
+ * SwiGLU of the MLP, elementwise over n bf16 values (n a multiple of 8):
+ * Y = silu(U) * V with silu(u) = u / (1 + exp(-u)), fp32 arithmetic; and its
+ * backward dU = dY * V * silu'(U), dV = dY * silu(U).  Outputs must not
+ * overlap inputs.
+ */
+int dd_swiglu_fwd(const void *U, const void *V, void *Y, long long n, void *stream);
+int dd_swiglu_bwd(const void *U, const void *V, const void *dY, void *dU, void *dV, long long n,
+                  void *stream);
+
 /* Workspace bytes dd_attn_bwd needs for this shape (0 for an invalid shape). */
 size_t dd_attn_bwd_workspace_bytes(int B, int L, int H, int D);
 

@@ -25,6 +25,15 @@ SIGNATURES = {
                                         _P, _I, ctypes.c_float, _I, _P, ctypes.c_size_t, _P]),
     "dd_rope": (ctypes.c_int, [_P, _P, _I, _I, _I, _I, ctypes.c_float, _I, _P, _I, _I, _P]),
     "dd_attn_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I, _I]),
+    "dd_gemm": (ctypes.c_int, [_P, ctypes.c_longlong, _I, _P, ctypes.c_longlong, _I, _P, _P,
+                               ctypes.c_longlong, _I, _I, _I, _P, ctypes.c_size_t, _P]),
+    "dd_gemm_workspace_bytes": (ctypes.c_size_t, [_I, _I, _I]),
+    "dd_layernorm_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _I, _I, ctypes.c_float, _P]),
+    "dd_layernorm_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _P,
+                                        ctypes.c_size_t, _P]),
+    "dd_layernorm_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I]),
+    "dd_swiglu_fwd": (ctypes.c_int, [_P, _P, _P, ctypes.c_longlong, _P]),
+    "dd_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_longlong, _P]),
     "dd_doclens_check": (ctypes.c_int, [_P, _I, ctypes.c_longlong]),
     "dd_status_str": (ctypes.c_char_p, [_I]),
     "dd_prof_enable": (ctypes.c_int, [_I]),

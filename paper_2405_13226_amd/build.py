@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libdd_attn.so")
 
 ARCH = "gfx950"
 HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_dkdv.hip", "dd_bwd_short.hip", "dd_prof.hip",
-               "dd_rope.hip", "dd_noalloc.hip"]
+               "dd_rope.hip", "dd_noalloc.hip", "dd_gemm.hip", "dd_block.hip"]
 # Extra flags per source.  The D = 128 dK/dV kernel and the one-kernel
 # short-row backward are scheduled for instruction-level parallelism
 # (measured: dK/dV ~6% faster at L = 8192, neutral at L = 256; short-row

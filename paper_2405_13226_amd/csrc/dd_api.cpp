@@ -271,6 +271,196 @@ int dd_attn_bwd_rope(const void *Q, const void *K, const void *V, const void *O,
                             workspace, workspace_bytes, stream);
 }
 
+size_t dd_gemm_workspace_bytes(int M, int N, int K)
+{
+    if (M < 256 || N < 256 || K < 64 || M % 256 || N % 256 || K % 64)
+        return 0;
+    return dd::gemm_workspace_bytes(M, N, K, dd::gemm_splits(M, N, K));
+}
+
+int dd_gemm(const void *A, long long lda, int trans_a, const void *B, long long ldb, int trans_b,
+            const void *R, void *C, long long ldc, int M, int N, int K, void *workspace,
+            size_t workspace_bytes, void *stream)
+{
+    if (!A || !B || !C)
+        return DD_ERR_NULL;
+    if (M < 256 || N < 256 || K < 64 || M % 256 || N % 256 || K % 64 || (trans_a && trans_b))
+        return DD_ERR_SHAPE;
+    const long long a_rows = trans_a ? K : M, a_cols = trans_a ? M : K;
+    const long long b_rows = trans_b ? N : K, b_cols = trans_b ? K : N;
+    if (lda < a_cols || ldb < b_cols || ldc < N)
+        return DD_ERR_SHAPE;
+    if (lda % 8 || ldb % 8 || ldc % 8 || !aligned(A, 16) || !aligned(B, 16) || !aligned(C, 16) ||
+        (R && !aligned(R, 16)))
+        return DD_ERR_ALIGN;
+    const int splits = dd::gemm_splits(M, N, K);
+    const size_t need = dd::gemm_workspace_bytes(M, N, K, splits);
+    if (need && (!workspace || workspace_bytes < need))
+        return DD_ERR_WORKSPACE;
+    if (need && !aligned(workspace, 16))
+        return DD_ERR_ALIGN;
+    Range ra = range_of(A, static_cast<size_t>((a_rows - 1) * lda + a_cols) * 2);
+    Range rb = range_of(B, static_cast<size_t>((b_rows - 1) * ldb + b_cols) * 2);
+    const size_t cbytes = static_cast<size_t>((static_cast<long long>(M) - 1) * ldc + N) * 2;
+    Range rc = range_of(C, cbytes), rr = range_of(R, R ? cbytes : 0);
+    Range rw = range_of(workspace, need);
+    if (overlaps(rc, ra) || overlaps(rc, rb) || overlaps(rw, ra) || overlaps(rw, rb) ||
+        overlaps(rw, rc) || overlaps(rw, rr) || (R && R != C && overlaps(rr, rc)))
+        return DD_ERR_ALIAS;
+    dd::GemmArgs a{A, B, C, R, lda, ldb, ldc, M, N, K, trans_a != 0, trans_b != 0, splits,
+                   workspace, stream};
+    return dd::launch_gemm(a);
+}
+
+namespace {
+
+int check_ln(const void *X, int rows, int d)
+{
+    if (!X)
+        return DD_ERR_NULL;
+    if (rows < 1 || (d != 512 && d != 1024 && d != 2048) ||
+        static_cast<long long>(rows) * d >= (1LL << 40))
+        return DD_ERR_SHAPE;
+    return DD_OK;
+}
+
+}  // namespace
+
+size_t dd_layernorm_bwd_workspace_bytes(int rows, int d)
+{
+    if (check_ln(reinterpret_cast<const void *>(1), rows, d) != DD_OK)
+        return 0;
+    return dd::layernorm_workspace_bytes(rows, d);
+}
+
+int dd_layernorm_fwd(const void *X, const void *w, const void *b, void *Y, float *mean,
+                     float *rstd, int rows, int d, float eps, void *stream)
+{
+    int st = check_ln(X, rows, d);
+    if (st != DD_OK)
+        return st;
+    if (!w || !b || !Y || !mean || !rstd)
+        return DD_ERR_NULL;
+    if (!(std::isfinite(eps) && eps > 0.0f))
+        return DD_ERR_SHAPE;
+    for (const void *p : std::initializer_list<const void *>{X, w, b, Y})
+        if (!aligned(p, 16))
+            return DD_ERR_ALIGN;
+    if (!aligned(mean, 4) || !aligned(rstd, 4))
+        return DD_ERR_ALIGN;
+    const size_t tb = static_cast<size_t>(rows) * d * 2, vb = static_cast<size_t>(d) * 2,
+                 sb = static_cast<size_t>(rows) * 4;
+    Range ins[] = {range_of(X, tb), range_of(w, vb), range_of(b, vb)};
+    Range outs[] = {range_of(Y, tb), range_of(mean, sb), range_of(rstd, sb)};
+    for (int i = 0; i < 3; ++i) {
+        for (Range in : ins)
+            if (overlaps(outs[i], in))
+                return DD_ERR_ALIAS;
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(outs[i], outs[j]))
+                return DD_ERR_ALIAS;
+    }
+    dd::LayerNormArgs a{};
+    a.X = X;
+    a.w = w;
+    a.b = b;
+    a.Y = Y;
+    a.mean = mean;
+    a.rstd = rstd;
+    a.rows = rows;
+    a.d = d;
+    a.eps = eps;
+    a.stream = stream;
+    return dd::launch_layernorm_fwd(a);
+}
+
+int dd_layernorm_bwd(const void *X, const void *w, const float *mean, const float *rstd,
+                     const void *dY, const void *dRes, void *dX, void *dw, void *db, int rows,
+                     int d, void *workspace, size_t workspace_bytes, void *stream)
+{
+    int st = check_ln(X, rows, d);
+    if (st != DD_OK)
+        return st;
+    if (!w || !mean || !rstd || !dY || !dX || !dw || !db)
+        return DD_ERR_NULL;
+    const size_t need = dd::layernorm_workspace_bytes(rows, d);
+    if (!workspace || workspace_bytes < need)
+        return DD_ERR_WORKSPACE;
+    for (const void *p : std::initializer_list<const void *>{X, w, dY, dX, dw, db, workspace})
+        if (!aligned(p, 16))
+            return DD_ERR_ALIGN;
+    if ((dRes && !aligned(dRes, 16)) || !aligned(mean, 4) || !aligned(rstd, 4) ||
+        !aligned(dw, 2) || !aligned(db, 2))
+        return DD_ERR_ALIGN;
+    const size_t tb = static_cast<size_t>(rows) * d * 2, vb = static_cast<size_t>(d) * 2,
+                 sb = static_cast<size_t>(rows) * 4;
+    Range ins[] = {range_of(X, tb), range_of(w, vb), range_of(mean, sb), range_of(rstd, sb),
+                   range_of(dY, tb), range_of(dRes, dRes ? tb : 0)};
+    Range outs[] = {range_of(dX, tb), range_of(dw, vb), range_of(db, vb),
+                    range_of(workspace, need)};
+    for (int i = 0; i < 4; ++i) {
+        for (Range in : ins)
+            if (overlaps(outs[i], in))
+                return DD_ERR_ALIAS;
+        for (int j = i + 1; j < 4; ++j)
+            if (overlaps(outs[i], outs[j]))
+                return DD_ERR_ALIAS;
+    }
+    dd::LayerNormArgs a{};
+    a.X = X;
+    a.w = w;
+    a.mean_in = mean;
+    a.rstd_in = rstd;
+    a.dY = dY;
+    a.dRes = dRes;
+    a.dX = dX;
+    a.dw = dw;
+    a.db = db;
+    a.workspace = workspace;
+    a.rows = rows;
+    a.d = d;
+    a.stream = stream;
+    return dd::launch_layernorm_bwd(a);
+}
+
+int dd_swiglu_fwd(const void *U, const void *V, void *Y, long long n, void *stream)
+{
+    if (!U || !V || !Y)
+        return DD_ERR_NULL;
+    if (n < 8 || n % 8 || n >= (1LL << 40))
+        return DD_ERR_SHAPE;
+    if (!aligned(U, 16) || !aligned(V, 16) || !aligned(Y, 16))
+        return DD_ERR_ALIGN;
+    const size_t tb = static_cast<size_t>(n) * 2;
+    Range ry = range_of(Y, tb);
+    if (overlaps(ry, range_of(U, tb)) || overlaps(ry, range_of(V, tb)))
+        return DD_ERR_ALIAS;
+    dd::SwigluArgs a{U, V, nullptr, Y, nullptr, nullptr, n, false, stream};
+    return dd::launch_swiglu(a);
+}
+
+int dd_swiglu_bwd(const void *U, const void *V, const void *dY, void *dU, void *dV, long long n,
+                  void *stream)
+{
+    if (!U || !V || !dY || !dU || !dV)
+        return DD_ERR_NULL;
+    if (n < 8 || n % 8 || n >= (1LL << 40))
+        return DD_ERR_SHAPE;
+    for (const void *p : std::initializer_list<const void *>{U, V, dY, dU, dV})
+        if (!aligned(p, 16))
+            return DD_ERR_ALIGN;
+    const size_t tb = static_cast<size_t>(n) * 2;
+    Range ins[] = {range_of(U, tb), range_of(V, tb), range_of(dY, tb)};
+    Range rdu = range_of(dU, tb), rdv = range_of(dV, tb);
+    for (Range in : ins)
+        if (overlaps(rdu, in) || overlaps(rdv, in))
+            return DD_ERR_ALIAS;
+    if (overlaps(rdu, rdv))
+        return DD_ERR_ALIAS;
+    dd::SwigluArgs a{U, V, dY, nullptr, dU, dV, n, true, stream};
+    return dd::launch_swiglu(a);
+}
+
 int dd_rope(const void *X, void *Y, int B, int L, int H, int D, float base, int inverse,
             const int32_t *cu_doclens, int n_docs, int doc_positions, void *stream)
 {

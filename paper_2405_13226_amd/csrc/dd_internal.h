@@ -64,6 +64,49 @@ constexpr size_t kNoAllocScratchBytes = static_cast<size_t>(16) << 20;
 // device with the device current).  Returns DD_OK or DD_ERR_HIP.
 int noalloc_scratch(void **ptr);
 
+// C[M, N] = op(A) op(B) (dd_gemm.hip); M and N multiples of 256, K of 64.
+struct GemmArgs {
+    const void *A, *B;
+    void *C;
+    const void *R;            // optional residual added to C (bf16, row stride ldc)
+    long long lda, ldb, ldc;  // row strides in elements
+    int M, N, K;
+    bool trans_a, trans_b;    // A stored [K][M]; B stored [N][K] (not both)
+    int splits;               // K splits (1: none); > 1 needs the workspace
+    void *workspace;          // fp32 [splits][M][N]
+    void *stream;
+};
+int gemm_splits(int M, int N, int K);
+size_t gemm_workspace_bytes(int M, int N, int K, int splits);
+int launch_gemm(const GemmArgs &a);
+
+// LayerNorm over rows of d elements (dd_block.hip), d in {512, 1024, 2048}.
+struct LayerNormArgs {
+    const void *X, *w, *b;    // [rows, d] input; weight and bias [d]
+    void *Y;                  // forward output [rows, d]
+    float *mean, *rstd;       // forward outputs [rows]
+    const float *mean_in, *rstd_in;
+    const void *dY, *dRes;    // backward input; optional residual gradient
+    void *dX, *dw, *db;       // backward outputs
+    void *workspace;          // fp32 column partials
+    int rows, d;
+    float eps;
+    void *stream;
+};
+size_t layernorm_workspace_bytes(int rows, int d);
+int launch_layernorm_fwd(const LayerNormArgs &a);
+int launch_layernorm_bwd(const LayerNormArgs &a);
+
+// SwiGLU y = silu(u) v over n elements (n a multiple of 8), and its backward.
+struct SwigluArgs {
+    const void *U, *V, *dY;
+    void *Y, *dU, *dV;
+    long long n;
+    bool backward;
+    void *stream;
+};
+int launch_swiglu(const SwigluArgs &a);
+
 // Both return a dd_status value (DD_OK or DD_ERR_HIP).
 int launch_fwd(const FwdArgs &a);
 int launch_bwd(const BwdArgs &a);

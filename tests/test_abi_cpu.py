@@ -204,6 +204,43 @@ def test_fused_rope_forward_validation(lib):
     assert call({5: fake(4)}) == ALIAS          # Q_rot overlaps LSE
 
 
+def test_block_kernel_validation(lib):
+    # GEMM: shapes, strides, alignment, aliasing; rejected on the host.
+    def gemm(A=None, B=None, C=None, R=None, M=256, N=256, K=64, lda=None, ldb=None, ldc=None,
+             ta=0, tb=0, ws=None, wsb=0):
+        lda = lda if lda is not None else (M if ta else K)
+        ldb = ldb if ldb is not None else (K if tb else N)
+        ldc = ldc if ldc is not None else N
+        return lib.dd_gemm(A or fake(0), lda, ta, B or fake(1), ldb, tb, R, C or fake(2), ldc,
+                           M, N, K, ws, wsb, None)
+    assert lib.dd_gemm(None, 64, 0, fake(1), 256, 0, None, fake(2), 256, 256, 256, 64, None, 0,
+                       None) == NULL
+    for kw in (dict(M=255), dict(N=300), dict(K=96), dict(M=0), dict(ta=1, tb=1),
+               dict(lda=32), dict(ldc=128)):
+        assert gemm(**kw) == SHAPE, kw
+    assert gemm(lda=68) == ALIGN
+    assert gemm(A=fake(0, 8)) == ALIGN
+    assert gemm(C=fake(0, 1024)) == ALIAS           # C overlaps A
+    assert gemm(R=fake(2, 64)) == ALIAS             # R partly overlaps C
+    assert lib.dd_gemm_workspace_bytes(255, 256, 64) == 0
+    # LayerNorm
+    ln = lambda **kw: lib.dd_layernorm_fwd(kw.get("X", fake(0)), fake(1), fake(2),
+                                           kw.get("Y", fake(3)), fake(4), fake(5),
+                                           kw.get("rows", 8), kw.get("d", 512),
+                                           kw.get("eps", 1e-5), None)
+    assert ln(X=None) == NULL
+    assert ln(d=256) == SHAPE and ln(d=4096) == SHAPE and ln(rows=0) == SHAPE
+    assert ln(eps=0.0) == SHAPE and ln(eps=float("nan")) == SHAPE
+    assert ln(Y=fake(0, 64)) == ALIAS
+    assert lib.dd_layernorm_bwd_workspace_bytes(8, 300) == 0
+    assert lib.dd_layernorm_bwd(fake(0), fake(1), fake(2), fake(3), fake(4), None, fake(5),
+                                fake(6), fake(7), 8, 512, fake(8), 0, None) == WORKSPACE
+    # SwiGLU
+    assert lib.dd_swiglu_fwd(fake(0), fake(1), fake(2), 12, None) == SHAPE
+    assert lib.dd_swiglu_fwd(fake(0), fake(1), fake(0, 16), 64, None) == ALIAS
+    assert lib.dd_swiglu_bwd(fake(0), fake(1), fake(2), fake(3), fake(3, 16), 64, None) == ALIAS
+
+
 def test_noalloc_backward_validation(lib):
     # Rejected on the host before the device scratch is touched.
     SCRATCH = 9

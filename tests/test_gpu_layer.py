@@ -1,5 +1,5 @@
-"""GPU parity of one OpenLM block (paper_2405_13226_amd/layer.py: library
-attention and RoPE kernels, vendor GEMMs) against the fp64 block oracle
+"""GPU parity of one OpenLM block (paper_2405_13226_amd/layer.py: every step
+in this library's kernels) against the fp64 block oracle
 (oracle/layer.py), forward output and the gradients of sum(dy * y) with
 respect to the input and every weight.
 
@@ -12,6 +12,11 @@ roundings give relative errors of order 6e-3 and 9e-3; the bound is about
 twice that.  A plain torch bf16 implementation of the same block (attention in
 fp32 through torch) measured 0.9% (output) and 1.0-1.3% (gradients) against
 the same oracle on the first case, the library block the same to two digits.
+The weights are N(0, (0.1 sqrt(256 / d))^2), which keeps the projections'
+magnitude, and so the sharpness of the softmax that amplifies the rounding
+of q and k, at that of d = 256; the test also runs that plain torch bf16
+block (torch GEMMs, LayerNorm, SiLU; library attention) on the same inputs
+and requires the library block's error to stay within 1.2x of it (+2e-3).
 """
 import numpy as np
 import pytest
@@ -30,30 +35,54 @@ LAYER_RTOL = 2e-2
 def run_block(cuda, B, L, d, H, hidden, base, cu=None, doc_pos=False, seed=0):
     from paper_2405_13226_amd.layer import OpenLMBlock
     log(f"block B={B} L={L} d={d} H={H} hidden={hidden} base={base} docs={cu is not None} doc_pos={doc_pos}")
-    blk = OpenLMBlock(d, H, hidden, base, device=cuda, seed=seed, init_scale=0.1)
+    blk = OpenLMBlock(d, H, hidden, base, device=cuda, seed=seed,
+                      init_scale=0.1 * (256 / d) ** 0.5)
     with torch.no_grad():  # non-trivial norm parameters
         for n in ("ln1_w", "ln2_w"):
             getattr(blk, n).add_(torch.randn(d, device=cuda).to(torch.bfloat16) * 0.2)
         for n in ("ln1_b", "ln2_b"):
             getattr(blk, n).add_(torch.randn(d, device=cuda).to(torch.bfloat16) * 0.2)
-    x = to_dev(synth.normal_bf16((B, L, d), seed, 21), cuda).requires_grad_(True)
+    x0 = to_dev(synth.normal_bf16((B, L, d), seed, 21), cuda)
     dy = to_dev(synth.normal_bf16((B, L, d), seed, 22), cuda)
-    y = blk(x, cu, doc_pos)
-    y.backward(dy)
-    torch.cuda.synchronize()
     w = {n: to_f64(p.detach()) for n, p in blk.weights().items()}
-    y_ref, g_ref = OL.block_fwd_bwd(to_f64(x.detach()), w, to_f64(dy), H, base, cu, doc_pos)
-    res = {"y": rel_l2(to_f64(y.detach()), y_ref), "x": rel_l2(to_f64(x.grad), g_ref["x"])}
-    for n, p in blk.weights().items():
-        res[n] = rel_l2(to_f64(p.grad), g_ref[n])
-    log("  " + "  ".join(f"{k}={v:.3g}" for k, v in res.items()))
-    for k, v in res.items():
+    y_ref, g_ref = OL.block_fwd_bwd(to_f64(x0), w, to_f64(dy), H, base, cu, doc_pos)
+    out = {}
+    for name, fn in (("library", lambda x: blk(x, cu, doc_pos)),
+                     ("torch", lambda x: torch_block(blk, x, cu, doc_pos))):
+        blk.zero_grad(set_to_none=True)
+        x = x0.clone().requires_grad_(True)
+        y = fn(x)
+        y.backward(dy)
+        torch.cuda.synchronize()
+        res = {"y": rel_l2(to_f64(y.detach()), y_ref), "x": rel_l2(to_f64(x.grad), g_ref["x"])}
+        for n, p in blk.weights().items():
+            res[n] = rel_l2(to_f64(p.grad), g_ref[n])
+        log(f"  {name}: " + "  ".join(f"{k}={v:.3g}" for k, v in res.items()))
+        out[name] = res
+    for k, v in out["library"].items():
         assert v <= LAYER_RTOL, (k, v)
-    return res
+        assert v <= 1.2 * out["torch"][k] + 2e-3, (k, v, out["torch"][k])
+    return out["library"]
 
 
-@pytest.mark.parametrize("B,L,d,H,hidden,base", [(2, 192, 256, 2, 704, 10000.0),
-                                                 (1, 300, 128, 2, 352, 100000.0)])
+def torch_block(blk, x, cu, doc_pos):
+    """The same block with torch's bf16 GEMMs, LayerNorm and SiLU around the
+    library's attention (the reference the error is compared with)."""
+    import torch.nn.functional as F
+    from paper_2405_13226_amd.attention import attention
+    B, L, d = x.shape
+    H, D = blk.H, blk.D
+    t = x.reshape(B * L, d)
+    a = F.layer_norm(t, (d,), blk.ln1_w, blk.ln1_b, 1e-5)
+    q, k, v = (s.reshape(B, L, H, D).contiguous() for s in (a @ blk.w_qkv).split(d, dim=-1))
+    o = attention(q, k, v, True, cu, blk.rope_base, doc_pos)
+    h = t + o.reshape(B * L, d) @ blk.w_o
+    m = F.layer_norm(h, (d,), blk.ln2_w, blk.ln2_b, 1e-5)
+    return (h + (F.silu(m @ blk.w_1) * (m @ blk.w_3)) @ blk.w_2).reshape(B, L, d)
+
+
+@pytest.mark.parametrize("B,L,d,H,hidden,base", [(2, 256, 512, 4, 768, 10000.0),
+                                                 (1, 512, 512, 8, 1280, 100000.0)])
 def test_block_parity(cuda, B, L, d, H, hidden, base):
     run_block(cuda, B, L, d, H, hidden, base, seed=L)
 
@@ -62,4 +91,4 @@ def test_block_parity_masked_chunk_document_positions(cuda):
     B, L = 2, 256
     lens = synth.lognormal_doc_lengths(4, total_tokens=B * L, median=80, sigma=1.0)
     cu = dd.chunk_doclens(lens, B * L)
-    run_block(cuda, B, L, 256, 2, 704, 10000.0, cu, True, seed=3)
+    run_block(cuda, B, L, 512, 4, 768, 10000.0, cu, True, seed=3)
