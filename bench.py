@@ -155,7 +155,7 @@ def measured_traffic(workload, kernel, group=None):
     with open(path) as f:
         for line in f:
             if "=" in line and not line.lstrip().startswith("#"):
-                k, v = line.split("=", 1)
+                k, v = line.rsplit("=", 1)  # group names may hold "=" ("L=8192")
                 kv[k.strip()] = v.strip()
     if kv.get("source_hash") != kernel_source_hash():
         return None

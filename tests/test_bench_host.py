@@ -32,7 +32,7 @@ def _write_counters(path, counter, rows):
             w.writerow([i + 1, name, counter, kib])
 
 
-def test_traffic_summary_scales_by_the_copy(tmp_path):
+def test_traffic_summary_scales_by_the_copy(tmp_path, monkeypatch):
     # --buckets 8192,4096 of the D=64 sweep: per step forward, dQ, dK/dV per
     # group; one warm-up and one timed step.  The copies read half their
     # bytes (FETCH) and write all of them (WRITE), as measured on gfx950.
@@ -58,3 +58,11 @@ def test_traffic_summary_scales_by_the_copy(tmp_path):
     assert int(kv["fetch_bytes_per_launch.backward_dkdv.L=4096"]) == 3 * 500 * 1024 * 2
     assert int(kv["write_bytes_per_launch.backward_dkdv.L=4096"]) == 3 * 250 * 1024
     assert int(kv["bytes_per_launch.forward.L=8192"]) == 1000 * 1024 * 2 + 500 * 1024
+    # bench.measured_traffic reads such keys back (group names hold "=")
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    (prof / "traffic_dd_sweep_d64.txt").write_text(out)
+    h = bench.kernel_source_hash()  # the summary was stamped with the current sources
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: h)
+    assert bench.measured_traffic("dd_sweep_d64", "backward_dkdv", "L=4096") == 3 * 500 * 1024 * 2 + 3 * 250 * 1024
