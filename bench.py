@@ -25,6 +25,10 @@ Workloads (``--workload``):
                  forward + backward per bucket L = 256 .. 8192 at 65,536
                  tokens: step time, attention's share of it, and the fit
                  t(L) = alpha + beta * L (value: block TFLOP/s)
+  gemm_1b        the bf16 GEMMs of one OpenLM-1B block step at 65,536 tokens
+                 (forward, input-gradient and weight-gradient shapes), the
+                 library's dd_gemm timed beside torch.matmul (the vendor
+                 library) on the same operands
   tiny           B = 4, L = 256, H = 4, D = 64
 
 Prints ONE JSON line on stdout: the metric is useful attention TFLOP/s
@@ -170,7 +174,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="dd_sweep_d64",
                     choices=["dd_sweep_d64", "dd_sweep_d128", "chunk_vs_dd", "stream",
-                             "curriculum", "rope_d128", "rope_d128_fused", "layer_1b", "tiny"])
+                             "curriculum", "rope_d128", "rope_d128_fused", "layer_1b", "gemm_1b",
+                             "tiny"])
     ap.add_argument("--buckets", default=None,
                     help="comma-separated subset of bucket lengths (sweeps only)")
     ap.add_argument("--seed", type=int, default=0)
@@ -566,6 +571,8 @@ def main():
     buckets = [int(x) for x in args.buckets.split(",")] if args.buckets else None
     if args.workload == "layer_1b":
         return run_layer(args, buckets, dev)
+    if args.workload == "gemm_1b":
+        return run_gemm(args, dev)
     result, groups = run_workload(args.workload, args, buckets, dev, args.seed)
 
     extras = {}
@@ -667,6 +674,71 @@ def run_layer(args, buckets, dev):
         "groups": per,
         "fit": dict(alpha_ms=round(float(alpha), 4), beta_us_per_token=round(float(beta) * 1e3, 5),
                     max_residual_ms=round(resid, 4)),
+    }
+    print(json.dumps(result), flush=True)
+
+
+def run_gemm(args, dev):
+    """dd_gemm on the block's shapes at 65,536 tokens, timed with events
+    beside torch.matmul (vendor library) on the same operands."""
+    import torch
+    from paper_2405_13226_amd import block_ops
+    from paper_2405_13226_amd.layer import OPENLM_1B
+
+    T, d, hid = TOKENS, OPENLM_1B["d"], OPENLM_1B["hidden"]
+    # (name, M, N, K, trans_a, trans_b): y = x W, dx = dy W^T, dW = x^T dy
+    shapes = [("qkv fwd", T, 3 * d, d, 0, 0), ("out fwd", T, d, d, 0, 0),
+              ("w1 fwd", T, hid, d, 0, 0), ("w2 fwd", T, d, hid, 0, 0),
+              ("qkv dx", T, d, 3 * d, 0, 1), ("w1 dx", T, d, hid, 0, 1),
+              ("w2 dx", T, hid, d, 0, 1), ("qkv dW", d, 3 * d, T, 1, 0),
+              ("w1 dW", d, hid, T, 1, 0), ("w2 dW", hid, d, T, 1, 0)]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    per, tot_ms, tot_fl, tot_ms_t = [], 0.0, 0.0, 0.0
+    for name, M, N, K, ta, tb in shapes:
+        a = torch.randn((K, M) if ta else (M, K), generator=gen, device=dev).to(torch.bfloat16)
+        b = torch.randn((N, K) if tb else (K, N), generator=gen, device=dev).to(torch.bfloat16)
+        c = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        at, bt = (a.t() if ta else a), (b.t() if tb else b)
+        fns = {"dd": lambda: block_ops.gemm(a, b, bool(ta), bool(tb), out=c),
+               "torch": lambda: torch.matmul(at, bt)}
+        ms = {}
+        for key, fn in fns.items():
+            for _ in range(args.warmup):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize(dev)
+            e0.record()
+            for _ in range(args.steps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize(dev)
+            ms[key] = e0.elapsed_time(e1) / args.steps
+        fl = 2.0 * M * N * K
+        rec = dict(name=name, M=M, N=N, K=K, trans_a=ta, trans_b=tb, ms=round(ms["dd"], 4),
+                   tflops=round(fl / (ms["dd"] * 1e-3) / 1e12, 1),
+                   torch_ms=round(ms["torch"], 4),
+                   torch_tflops=round(fl / (ms["torch"] * 1e-3) / 1e12, 1))
+        per.append(rec)
+        tot_ms += ms["dd"]
+        tot_ms_t += ms["torch"]
+        tot_fl += fl
+        log(f"  {name:8s} M={M} N={N} K={K}: dd {rec['ms']:.3f} ms {rec['tflops']:7.1f} TFLOP/s"
+            f" | torch {rec['torch_ms']:.3f} ms {rec['torch_tflops']:7.1f}")
+        del a, b, c
+    value = tot_fl / (tot_ms * 1e-3) / 1e12
+    result = {
+        "metric": "OpenLM-1B block GEMM TFLOP/s (dd_gemm) at 65,536 tokens",
+        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(tot_ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 on device)",
+        "config": dict(workload="gemm_1b", tokens=T, d=d, hidden=hid),
+        "groups": per,
+        "roofline": dict(bound="mfma", kernel="gemm", achieved=round(value, 2),
+                         peak=BF16_PEAK_TFLOPS, unit="TFLOP/s",
+                         frac=round(value / BF16_PEAK_TFLOPS, 4), traffic=None),
+        "torch_value": round(tot_fl / (tot_ms_t * 1e-3) / 1e12, 2),
     }
     print(json.dumps(result), flush=True)
 

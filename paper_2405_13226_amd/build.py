@@ -23,13 +23,14 @@ LIB = os.path.join(PKG, "libdd_attn.so")
 ARCH = "gfx950"
 HIP_SOURCES = ["dd_fwd.hip", "dd_bwd.hip", "dd_dkdv.hip", "dd_bwd_short.hip", "dd_prof.hip",
                "dd_rope.hip", "dd_noalloc.hip", "dd_gemm.hip", "dd_block.hip"]
-# Extra flags per source.  The D = 128 dK/dV kernel and the one-kernel
-# short-row backward are scheduled for instruction-level parallelism
-# (measured: dK/dV ~6% faster at L = 8192, neutral at L = 256; short-row
-# backward 11% faster at L = 64, 2% at L = 128 and 256); the default strategy
-# is faster for every other kernel.
+# Extra flags per source.  The D = 128 dK/dV kernel, the one-kernel
+# short-row backward and the GEMM are scheduled for instruction-level
+# parallelism (measured: dK/dV ~6% faster at L = 8192, neutral at L = 256;
+# short-row backward 11% faster at L = 64, 2% at L = 128 and 256; GEMM 4-6%
+# on the forward shapes, neutral on the others); the default strategy is
+# faster for every other kernel.
 _ILP = ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]
-HIP_SOURCE_FLAGS = {"dd_dkdv.hip": _ILP, "dd_bwd_short.hip": _ILP}
+HIP_SOURCE_FLAGS = {"dd_dkdv.hip": _ILP, "dd_bwd_short.hip": _ILP, "dd_gemm.hip": _ILP}
 CXX_SOURCES = ["dd_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 VALU forms are disabled for all device code.

@@ -39,8 +39,9 @@ namespace dd {
 
 struct GemmTile {
     static constexpr int BM = 256, BN = 256, BK = 64, NW = 8;
-    static constexpr int SUB = 64 * 64;       // elements of one 64 x 64 sub-tile
-    static constexpr int HALF = 4 * SUB;      // the A (or B) tile of one K step
+    static constexpr int SLAB = 16 * 64 + 32;  // one 16-column slab, padded by 64 bytes
+    static constexpr int SUB = 4 * SLAB;       // elements of one 64 x 64 sub-tile
+    static constexpr int HALF = 4 * SUB;       // the A (or B) tile of one K step
 };
 
 // TA: A is stored [K][M]; TB: B is stored [N][K]; PART: write an fp32
@@ -79,34 +80,33 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
     const int kbeg = static_cast<int>(blockIdx.y) * k_len;
     const int nkt = min(k_len, K - kbeg) / T::BK;
 
-    // LDS layouts of a 64 x 64 sub-tile (8 KiB, 512 slots of 16 bytes):
+    // LDS layouts of a 64 x 64 sub-tile (8 KiB of data):
     //  * reduction axis along the rows (A^T, B): tile_off<64>, read with the
-    //    transposing LDS read; slot q holds row q / 8, stored chunk q % 8;
+    //    transposing LDS read;
     //  * reduction axis along the columns (A, B^T): four slabs of 16 columns,
-    //    each 64 rows of 32 bytes; row r's half h of a slab is stored at half
+    //    each 64 rows of 32 bytes (SLAB elements apart, 64 bytes of padding
+    //    between slabs); row r's half h of a slab is stored at half
     //    h ^ ((r >> 3) & 1).  A lane's 8 consecutive k of sub-step kk are then
-    //    at a fixed offset plus kk * 1024 elements, and 16 lanes reading 16
-    //    consecutive rows cover the 64 banks once.
-    // Every lane loads slot q = 64 wave + lane (16 bytes) of each sub-tile
-    // per K step.  The host guarantees that every tile lies inside the
-    // matrices (M, N multiples of 256, K of 64): no load needs clamping.
-    const int q = wave * 64 + lane;
-    auto slot_off = [&](bool k_rows, long long ld) __attribute__((always_inline)) {
-        long long row, col;
-        if (k_rows) {
-            row = q >> 3;
-            col = 8 * ((q & 7) ^ swz<64>(q >> 3));
-        } else {
-            const int slab = q >> 7, ws = q & 127, r = ws >> 1;
-            row = r;
-            col = 16 * slab + 8 * ((ws & 1) ^ ((r >> 3) & 1));
-        }
-        return row * ld + col;
-    };
-    const uint16_t *pa = A + slot_off(TA, lda) +
+    //    at a fixed offset plus kk * SLAB elements, 16 lanes reading 16
+    //    consecutive rows cover the 64 banks once, and so do 16 lanes
+    //    writing two rows' 16 chunks (the padding shifts each slab by 16
+    //    banks).
+    // Every lane loads 16 bytes of each sub-tile per K step: row q / 8,
+    // chunk q % 8 (q = 64 wave + lane), so a load instruction reads eight
+    // whole 128-byte row pieces.  The host guarantees that every tile lies
+    // inside the matrices (M, N multiples of 256, K of 64): no load needs
+    // clamping.
+    const int q = wave * 64 + lane, qr = q >> 3, qc = q & 7;
+    const uint16_t *pa = A + qr * lda + qc * 8 +
                          (TA ? static_cast<long long>(kbeg) * lda + m0 : static_cast<long long>(m0) * lda + kbeg);
-    const uint16_t *pb = B + slot_off(!TB, ldb) +
+    const uint16_t *pb = B + qr * ldb + qc * 8 +
                          (TB ? static_cast<long long>(n0) * ldb + kbeg : static_cast<long long>(kbeg) * ldb + n0);
+    // LDS position of this lane's chunk in either layout.
+    auto lds_pos = [&](bool k_rows) __attribute__((always_inline)) {
+        return k_rows ? qr * 64 + 8 * (qc ^ swz<64>(qr))
+                      : (qc >> 1) * T::SLAB + qr * 16 + 8 * ((qc & 1) ^ ((qr >> 3) & 1));
+    };
+    const int wa = lds_pos(TA), wb = lds_pos(!TB);
     // Sub-tile s starts 64 rows (stored along the tile's rows) or 64 columns
     // further; K step kt moves 64 rows or columns.
     const long long sa = TA ? 64 : 64 * lda, sb = TB ? 64 * ldb : 64;
@@ -122,8 +122,8 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
     auto store = [&](uint16_t *stage) __attribute__((always_inline)) {
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-            *reinterpret_cast<u32x4 *>(stage + s * T::SUB + q * 8) = ra[s];
-            *reinterpret_cast<u32x4 *>(stage + T::HALF + s * T::SUB + q * 8) = rb[s];
+            *reinterpret_cast<u32x4 *>(stage + s * T::SUB + wa) = ra[s];
+            *reinterpret_cast<u32x4 *>(stage + T::HALF + s * T::SUB + wb) = rb[s];
         }
     };
 
@@ -140,12 +140,12 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
     };
     // Fragment i of A: rows (m) 32 i .. +31 of the wave's 128, sub-tile
     // 2 wm + i / 2; fragment j of B: columns 32 j .. +31 of the wave's 64,
-    // sub-tile wn.  Sub-step kk: + 1024 kk (slabs) or + 16 rows.
+    // sub-tile wn.  Sub-step kk: + SLAB kk (slabs) or + 16 rows.
     auto a_frag = [&](const uint16_t *at, int i, int kk) __attribute__((always_inline)) {
         const uint16_t *sub = at + (2 * wm + (i >> 1)) * T::SUB;
         const int mo = 32 * (i & 1);
         if constexpr (!TA)
-            return lds_row8(sub + kk * 1024 + row_off(mo));
+            return lds_row8(sub + kk * T::SLAB + row_off(mo));
         else
             return join(lds_tr4(sub + kk * 1024 + tr_off(mo, 0)),
                         lds_tr4(sub + kk * 1024 + tr_off(mo, 1)));
@@ -154,7 +154,7 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
         const uint16_t *sub = bt + wn * T::SUB;
         const int no = 32 * j;
         if constexpr (TB)
-            return lds_row8(sub + kk * 1024 + row_off(no));
+            return lds_row8(sub + kk * T::SLAB + row_off(no));
         else
             return join(lds_tr4(sub + kk * 1024 + tr_off(no, 0)),
                         lds_tr4(sub + kk * 1024 + tr_off(no, 1)));
@@ -191,7 +191,10 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
         }
         // reads per K step: A 16 row reads or 32 transposed halves, B 8 row
         // reads or 16 transposed halves
-        constexpr int kAhead = 8;
+#ifndef GEMM_AHEAD
+#define GEMM_AHEAD 8
+#endif
+        constexpr int kAhead = GEMM_AHEAD;
         constexpr int NR = (TA ? 32 : 16) + (TB ? 8 : 16);
         constexpr int NP = 32;
         constexpr int QR = (NR - kAhead) / NP, RR = (NR - kAhead) % NP;
