@@ -743,6 +743,24 @@ def run_gemm(args, dev):
     print(json.dumps(result), flush=True)
 
 
+def row_pairs(B, L, cu=None):
+    """Allowed causal (query, key) pairs of each of the B rows (one head)."""
+    import numpy as np
+    from paper_2405_13226_amd import dd as ddh
+    seg = ddh.segments(B, L, cu)
+    starts = np.concatenate([[0], np.cumsum(seg)[:-1]])
+    out = np.zeros(B, dtype=np.int64)
+    np.add.at(out, starts // L, seg * (seg + 1) // 2)
+    return out
+
+
+def sample_flops(pairs, B, L, D, cu=None):
+    """Useful forward + backward FLOPs (14 D per allowed pair) of the listed
+    (b, h) slices of a [B, L] batch."""
+    rp = row_pairs(B, L, cu)
+    return 14 * D * sum(int(rp[b]) for b, _ in pairs)
+
+
 def cpu_baseline(groups, result, args):
     """The fp64 oracle timed on a bounded sample of every distinct group of
     the workload: as many (b, h) pairs as the oracle has threads (all of
@@ -753,7 +771,6 @@ def cpu_baseline(groups, result, args):
     import numpy as np
     import oracle
     import synth
-    from paper_2405_13226_amd import dd as ddh
 
     cores = oracle.threads()
     seen, per_group = {}, []
@@ -789,10 +806,7 @@ def cpu_baseline(groups, result, args):
                 if secs >= 0.5 or grow < 2:
                     break
                 n *= grow
-            seg = ddh.segments(Bs, L, cu)
-            rows_pairs = int((seg * (seg + 1) // 2).sum())  # per head, over the Bs rows
-            sample_flops = 14 * D * rows_pairs * len(pairs) / H
-            rate = sample_flops / secs
+            rate = sample_flops(pairs, Bs, L, D, cu) / secs
             seen[key] = dict(pairs_timed=len(pairs), seconds=round(secs, 3), rate=rate)
             log(f"cpu oracle: {len(pairs)} (b,h) pairs of {g['name']} in {secs:.2f} s")
         m = seen[key]

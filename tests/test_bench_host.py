@@ -66,3 +66,13 @@ def test_traffic_summary_scales_by_the_copy(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     monkeypatch.setattr(bench, "kernel_source_hash", lambda: h)
     assert bench.measured_traffic("dd_sweep_d64", "backward_dkdv", "L=4096") == 3 * 500 * 1024 * 2 + 3 * 250 * 1024
+
+
+def test_cpu_baseline_counts_every_sampled_slice():
+    # 16 sampled (b, h) slices of full causal rows of 8192 tokens: 16 x
+    # 8192*8193/2 pairs; with documents, each row's own segments count.
+    pairs = [(0, h) for h in range(16)]
+    assert bench.sample_flops(pairs, 1, 8192, 64) == 14 * 64 * 16 * 8192 * 8193 // 2
+    cu = [0, 3, 10, 16]  # rows of 8: [0,3) [3,8) | [8,10) [10,16)
+    assert list(bench.row_pairs(2, 8, cu)) == [6 + 15, 3 + 21]
+    assert bench.sample_flops([(1, 0), (1, 5), (0, 2)], 2, 8, 64, cu) == 14 * 64 * (24 + 24 + 21)
