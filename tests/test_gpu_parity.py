@@ -73,6 +73,27 @@ def test_persistent_kernels_document_masked(cuda, D):
                tag=f"persistent D={D}, documents")
 
 
+# Rows of 129..256 tokens at D = 64 take the persistent one-kernel backward:
+# 256 workgroups (one per CU) walk the slices b*H + h, a workgroup's next
+# slice 256 further on, its inputs staged tile by tile during the previous
+# slice.  200 x 3 slices give two or three slices per workgroup; the sampled
+# slices 0, 256, 300, 512 and 599 are first, second and third slices of
+# their workgroups.  L = 200 leaves a ragged last query tile.
+SHORT_PERSIST_BH = [(0, 0), (85, 1), (100, 0), (170, 2), (199, 2)]
+
+
+@pytest.mark.parametrize("L", [200, 256])
+@pytest.mark.parametrize("mode", ["causal", "full", "docs"])
+def test_short_rows_persistent_several_slices(cuda, L, mode):
+    B, H = 200, 3
+    cu = None
+    if mode == "docs":
+        lens = synth.lognormal_doc_lengths(L, total_tokens=B * L, median=L / 3, sigma=0.8)
+        cu = dd.chunk_doclens(lens, B * L)
+    check_case(B, L, H, 64, causal=mode != "full", cu=cu, seed=500 + L, bh=SHORT_PERSIST_BH,
+               tag=f"persistent one-kernel backward L={L} {mode}")
+
+
 @pytest.mark.parametrize("B,L,D,causal", [(2, 700, 64, True), (2, 700, 128, False),
                                          (1, 2100, 64, True), (1, 2100, 128, True)])
 def test_large_scores_forward(cuda, B, L, D, causal):
