@@ -842,7 +842,7 @@ def traffic_summary(args):
 
     fam = {"fwd_kernel": "forward", "dq_kernel": "backward_dq", "dkdv1_kernel": "backward_dkdv",
            "dkdv_kernel": "backward_dkdv", "bwd_short_kernel": "backward_short",
-           "rope_kernel": "rope"}
+           "bwd_short_persist_kernel": "backward_short", "rope_kernel": "rope"}
 
     def read(d, counter):
         f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
@@ -871,7 +871,7 @@ def traffic_summary(args):
         scale = float(2 ** 30) / float(np.median(copies))
         lib_rows = []
         for n, v in rows:
-            m = re.search(r"dd::(\w+)<", n)
+            m = re.search(r"dd::(\w+)", n)
             if m and m.group(1) in fam:
                 lib_rows.append((fam[m.group(1)], v * scale))
         out[counter] = (scale, lib_rows)

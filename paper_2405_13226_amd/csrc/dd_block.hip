@@ -187,17 +187,52 @@ layernorm_bwd_kernel(const uint16_t *__restrict__ X, const uint16_t *__restrict_
     }
 }
 
-// dw, db (bf16 [d]) = sums over the nparts partial rows.
+// Column sums of the nparts partial rows, in two stages so that the 16 MB
+// of partials (65,536 rows, d = 2048) are read by many workgroups at once:
+// stage 1, workgroup (x, y) sums the partial rows of chunk y (every
+// kLnChunks-th group of rows) for columns 64 x .. +63 (one coalesced
+// 256-byte row piece per wave and row, the four waves taking every fourth
+// row, combined through LDS) into sums[y][..]; stage 2 adds the kLnChunks
+// chunk sums of a column and rounds dw, db to bf16.
+constexpr int kLnChunks = 32;
+
 __global__ void __launch_bounds__(256)
-layernorm_param_grad_kernel(const float *__restrict__ part, int nparts, int d,
-                            uint16_t *__restrict__ dW, uint16_t *__restrict__ dB)
+layernorm_param_chunk_kernel(const float *__restrict__ part, int nparts, int d,
+                             float *__restrict__ sums)
+{
+    __shared__ float red[4][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = static_cast<int>(blockIdx.x) * 64 + lane;
+    const int per = (nparts + kLnChunks - 1) / kLnChunks;
+    const int p0 = static_cast<int>(blockIdx.y) * per, p1 = min(p0 + per, nparts);
+    float s0 = 0.f, s1 = 0.f;
+    if (col < 2 * d) {
+        int p = p0 + wave;
+        for (; p + 4 < p1; p += 8) {
+            s0 += part[static_cast<long long>(p) * 2 * d + col];
+            s1 += part[static_cast<long long>(p + 4) * 2 * d + col];
+        }
+        if (p < p1)
+            s0 += part[static_cast<long long>(p) * 2 * d + col];
+    }
+    red[wave][lane] = s0 + s1;
+    __syncthreads();
+    if (wave == 0 && col < 2 * d)
+        sums[static_cast<long long>(blockIdx.y) * 2 * d + col] =
+            (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+}
+
+__global__ void __launch_bounds__(256)
+layernorm_param_grad_kernel(const float *__restrict__ sums, int d, uint16_t *__restrict__ dW,
+                            uint16_t *__restrict__ dB)
 {
     const int col = static_cast<int>(blockIdx.x) * 256 + threadIdx.x;
     if (col >= 2 * d)
         return;
     float s = 0.f;
-    for (int p = 0; p < nparts; ++p)
-        s += part[static_cast<long long>(p) * 2 * d + col];
+#pragma unroll 8
+    for (int c = 0; c < kLnChunks; ++c)
+        s += sums[static_cast<long long>(c) * 2 * d + col];
     const __bf16 v = static_cast<__bf16>(s);
     uint16_t *dst = col < d ? dW + col : dB + (col - d);
     *dst = __builtin_bit_cast(uint16_t, v);
@@ -263,8 +298,9 @@ template __global__ void layernorm_bwd_kernel<4>(DD_LNB_ARGS);
 
 size_t layernorm_workspace_bytes(int rows, int d)
 {
+    // The workgroups' partial rows, then the chunk sums.
     const long long nparts = (rows + kLnRowsPerWg - 1) / kLnRowsPerWg;
-    return static_cast<size_t>(nparts) * 2 * d * sizeof(float);
+    return static_cast<size_t>(nparts + kLnChunks) * 2 * d * sizeof(float);
 }
 
 int launch_layernorm_fwd(const LayerNormArgs &a)
@@ -303,8 +339,14 @@ int launch_layernorm_bwd(const LayerNormArgs &a)
     }
     if (e != hipSuccess)
         return DD_ERR_HIP;
+    float *sums = part + static_cast<long long>(nparts) * 2 * a.d;
+    e = launch_kernel(layernorm_param_chunk_kernel,
+                      dim3(static_cast<unsigned>((2 * a.d + 63) / 64), kLnChunks), dim3(256), st,
+                      static_cast<const float *>(part), nparts, a.d, sums);
+    if (e != hipSuccess)
+        return DD_ERR_HIP;
     e = launch_kernel(layernorm_param_grad_kernel, dim3(static_cast<unsigned>((2 * a.d + 255) / 256)),
-                      dim3(256), st, static_cast<const float *>(part), nparts, a.d,
+                      dim3(256), st, static_cast<const float *>(sums), a.d,
                       static_cast<uint16_t *>(a.dw), static_cast<uint16_t *>(a.db));
     return e == hipSuccess ? DD_OK : DD_ERR_HIP;
 }

@@ -68,6 +68,26 @@ def test_traffic_summary_scales_by_the_copy(tmp_path, monkeypatch):
     assert bench.measured_traffic("dd_sweep_d64", "backward_dkdv", "L=4096") == 3 * 500 * 1024 * 2 + 3 * 250 * 1024
 
 
+def test_traffic_summary_names_the_short_row_backward(tmp_path):
+    # --buckets 256 of the D=64 sweep: the forward and the one-kernel
+    # backward, whose persistent form is not a template.
+    def rows(per_kib):
+        r = [("void at::native::copy_kernel", 2 ** 20)] * 3
+        for _ in range(2):
+            r += [("void dd::fwd_kernel<64, true, false>(...)", 100.0 * per_kib),
+                  ("dd::bwd_short_persist_kernel(unsigned short const*, ...)", 300.0 * per_kib)]
+        return r
+    _write_counters(tmp_path / "f", "FETCH_SIZE", rows(1.0))
+    _write_counters(tmp_path / "w", "WRITE_SIZE", rows(1.0))
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--workload",
+                          "dd_sweep_d64", "--buckets", "256", "--traffic-summary",
+                          str(tmp_path / "f"), str(tmp_path / "w")],
+                         capture_output=True, text=True, check=True).stdout
+    kv = dict(l.split(" = ") for l in out.splitlines() if " = " in l and not l.startswith("#"))
+    assert int(kv["bytes_per_launch.backward_short.L=256"]) == 2 * 300 * 1024
+
+
 def test_cpu_baseline_counts_every_sampled_slice():
     # 16 sampled (b, h) slices of full causal rows of 8192 tokens: 16 x
     # 8192*8193/2 pairs; with documents, each row's own segments count.
