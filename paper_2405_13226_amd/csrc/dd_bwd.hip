@@ -209,28 +209,22 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     // dK (scaled, and with respect to the unrotated keys under RoPE) and dV
     // of the current item.
     auto store = [&]() __attribute__((always_inline)) {
-        if (!k_ok)
-            return;
-        if (rope != 0) {
+        if (k_ok && rope != 0) {
             // Keeps the frequency arithmetic here: hoisted out of the item
             // loop it would hold registers across every tile.
             int gl = g;
             asm volatile("" : "+v"(gl));
             rope_unrotate_acc<DB>(dk, rt, rope_position(it.b, L, my_k, cu, n_docs, rope), gl);
         }
-        uint16_t *dKb = dK + it.base + my_k * rs;
-        uint16_t *dVb = dV + it.base + my_k * rs;
+        // Every lane takes part in the store's lane exchange.
+        const long long row = k_ok ? my_k : 0;
+        uint16_t *dKb = dK + it.base + row * rs;
+        uint16_t *dVb = dV + it.base + row * rs;
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int rg = 0; rg < 4; ++rg) {
-                const int d = db * 32 + 8 * rg + 4 * g;
-                *reinterpret_cast<bf16x4 *>(dKb + d) =
-                    pack4(dk[db][4 * rg] * scale, dk[db][4 * rg + 1] * scale,
-                          dk[db][4 * rg + 2] * scale, dk[db][4 * rg + 3] * scale);
-                *reinterpret_cast<bf16x4 *>(dVb + d) = pack4(
-                    dv[db][4 * rg], dv[db][4 * rg + 1], dv[db][4 * rg + 2], dv[db][4 * rg + 3]);
-            }
+        for (int db = 0; db < DB; ++db) {
+            store_block_bf16(dKb + db * 32, dk[db], scale, g, k_ok);
+            store_block_bf16(dVb + db * 32, dv[db], 1.0f, g, k_ok);
+        }
     };
 
     setup(it);
@@ -535,9 +529,7 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     // dQ (scaled, and with respect to the unrotated queries under RoPE) of
     // the current item.
     auto store = [&]() __attribute__((always_inline)) {
-        if (!q_ok)
-            return;
-        if (rope != 0) {
+        if (q_ok && rope != 0) {
             // Keeps the frequency arithmetic here: hoisted out of the item
             // loop it would hold registers across every tile.
             int gl = g;
@@ -546,16 +538,11 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                          "+s"(r.r4), "+s"(r.r16));
             rope_unrotate_acc<DB>(dq, r, rope_position(it.b, L, my_q, cu, n_docs, rope), gl);
         }
-        uint16_t *dQb = dQ + it.base + my_q * rs;
+        // Every lane takes part in the store's lane exchange.
+        uint16_t *dQb = dQ + it.base + static_cast<long long>(q_ok ? my_q : 0) * rs;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int rg = 0; rg < 4; ++rg) {
-                const int d = db * 32 + 8 * rg + 4 * g;
-                *reinterpret_cast<bf16x4 *>(dQb + d) =
-                    pack4(dq[db][4 * rg] * scale, dq[db][4 * rg + 1] * scale,
-                          dq[db][4 * rg + 2] * scale, dq[db][4 * rg + 3] * scale);
-            }
+            store_block_bf16(dQb + db * 32, dq[db], scale, g, q_ok);
     };
 
     setup(it);

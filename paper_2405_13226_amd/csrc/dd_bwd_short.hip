@@ -148,37 +148,25 @@ __device__ __forceinline__ void short_dq(const uint16_t *ks, const uint16_t *dss
         acc = mfma32(a, bs, acc);
     }
     const int q = i0 + l32;
-    if (q < L) {
-        uint16_t *dQb = dQs + static_cast<long long>(q) * rs;
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-            const int d = db * 32 + 8 * rg + 4 * g;
-            *reinterpret_cast<bf16x4 *>(dQb + d) =
-                pack4(acc[4 * rg] * scale, acc[4 * rg + 1] * scale, acc[4 * rg + 2] * scale,
-                      acc[4 * rg + 3] * scale);
-        }
-    }
+    store_block_bf16(dQs + static_cast<long long>(min(q, L - 1)) * rs + db * 32, acc, scale, g,
+                     q < L);
 }
 
-// dK (scaled) and dV of this lane's key my_k.
+// dK (scaled) and dV of this lane's key my_k (stored only when ok: a key
+// inside the row; every lane takes part in the exchange).
 __device__ __forceinline__ void short_store_kv(const f32x16 (&dk)[2], const f32x16 (&dv)[2],
                                                uint16_t *__restrict__ dKs,
                                                uint16_t *__restrict__ dVs, int my_k, long long rs,
-                                               int g, float scale)
+                                               int g, float scale, bool ok)
 {
-    uint16_t *dKb = dKs + static_cast<long long>(my_k) * rs;
-    uint16_t *dVb = dVs + static_cast<long long>(my_k) * rs;
+    const long long row = ok ? my_k : 0;
+    uint16_t *dKb = dKs + row * rs;
+    uint16_t *dVb = dVs + row * rs;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-            const int d = db * 32 + 8 * rg + 4 * g;
-            *reinterpret_cast<bf16x4 *>(dKb + d) =
-                pack4(dk[db][4 * rg] * scale, dk[db][4 * rg + 1] * scale,
-                      dk[db][4 * rg + 2] * scale, dk[db][4 * rg + 3] * scale);
-            *reinterpret_cast<bf16x4 *>(dVb + d) =
-                pack4(dv[db][4 * rg], dv[db][4 * rg + 1], dv[db][4 * rg + 2], dv[db][4 * rg + 3]);
-        }
+    for (int db = 0; db < 2; ++db) {
+        store_block_bf16(dKb + db * 32, dk[db], scale, g, ok);
+        store_block_bf16(dVb + db * 32, dv[db], 1.0f, g, ok);
+    }
 }
 
 // ROWS (64 or 128) is the row capacity: ROWS / 32 waves of 32 keys, and LDS
@@ -306,8 +294,7 @@ bwd_short_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         }
     }
 
-    if (k_ok)
-        short_store_kv(dk, dv, dK + base, dV + base, my_k, rs, g, scale);
+    short_store_kv(dk, dv, dK + base, dV + base, my_k, rs, g, scale, k_ok);
 }
 
 // -rowsum(dO * O) of one 8-element chunk pair, summed over the eight lanes
@@ -513,8 +500,7 @@ bwd_short_persist_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restr
             }
         }
 
-        if (k_ok)
-            short_store_kv(dk, dv, dK + base, dV + base, my_k, rs, g, scale);
+        short_store_kv(dk, dv, dK + base, dV + base, my_k, rs, g, scale, k_ok);
         if (!more)
             break;
         __syncthreads();  // every tile and dQ pass of this slice is done

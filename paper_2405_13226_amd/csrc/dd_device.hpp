@@ -167,6 +167,40 @@ __device__ __forceinline__ float halves_sum(float v)
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Stores a 32-element block of one row held in the matrix-core C layout
+// (register 4*rg + e of lane (l32, g) is element 8*rg + 4*g + e of row l32),
+// scaled and rounded to bf16, as 16-byte pieces: lanes l and l + 32 swap the
+// halves of each pair of 8-element groups (v_permlane32_swap), after which
+// lane g holds elements 8*rg .. 8*rg + 7 for rg = g and g + 2.  A store
+// instruction then writes 32 contiguous bytes per row instead of 8.  `dst`
+// points at element 0 of the block in this lane's row (16-byte aligned);
+// every lane of the wave takes part in the exchange, and only lanes with
+// `ok` store.
+__device__ __forceinline__ void store_block_bf16(uint16_t *dst, const f32x16 &acc, float scale,
+                                                 int g, bool ok)
+{
+#pragma unroll
+    for (int rp = 0; rp < 2; ++rp) {
+        const int r0 = 2 * rp, r1 = 2 * rp + 1;
+        const bf16x4 a = pack4(acc[4 * r0] * scale, acc[4 * r0 + 1] * scale,
+                               acc[4 * r0 + 2] * scale, acc[4 * r0 + 3] * scale);
+        const bf16x4 b = pack4(acc[4 * r1] * scale, acc[4 * r1 + 1] * scale,
+                               acc[4 * r1 + 2] * scale, acc[4 * r1 + 3] * scale);
+        const u32x2 ua = __builtin_bit_cast(u32x2, a), ub = __builtin_bit_cast(u32x2, b);
+        const u32x2 give = g ? ua : ub, keep = g ? ub : ua;
+        u32x2 got;
+#pragma unroll
+        for (int w = 0; w < 2; ++w) {
+            const auto r = __builtin_amdgcn_permlane32_swap(give[w], give[w], false, false);
+            got[w] = g ? r[0] : r[1];
+        }
+        const u32x4 piece = g ? u32x4{got[0], got[1], keep[0], keep[1]}
+                              : u32x4{keep[0], keep[1], got[0], got[1]};
+        if (ok)
+            *reinterpret_cast<u32x4 *>(dst + 8 * (g ? r1 : r0)) = piece;
+    }
+}
+
 // Wave-wide min / max of an int.
 __device__ __forceinline__ int wave_min(int v)
 {

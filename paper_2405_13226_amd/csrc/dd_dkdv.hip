@@ -302,9 +302,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     // dK (scaled, and with respect to the unrotated keys under RoPE) and dV
     // of the current item.
     auto store = [&]() __attribute__((always_inline)) {
-        if (!k_ok)
-            return;
-        if (!role_a && rope != 0) {
+        if (k_ok && !role_a && rope != 0) {
             // Keeps the frequency arithmetic here: hoisted out of the item
             // loop it would hold ~24 registers across every tile.
             int gl = g;
@@ -313,17 +311,12 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                          "+s"(r.r4), "+s"(r.r16));
             rope_unrotate_acc<DB>(acc, r, rope_position(it.b, L, my_k, cu, n_docs, rope), gl);
         }
+        // Every lane takes part in the store's lane exchange.
         const float osc = role_a ? 1.0f : scale;
-        uint16_t *dst = (role_a ? dV : dK) + it.base + my_k * rs;
+        uint16_t *dst = (role_a ? dV : dK) + it.base + static_cast<long long>(k_ok ? my_k : 0) * rs;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int rg = 0; rg < 4; ++rg) {
-                const int d = db * 32 + 8 * rg + 4 * g;
-                *reinterpret_cast<bf16x4 *>(dst + d) =
-                    pack4(acc[db][4 * rg] * osc, acc[db][4 * rg + 1] * osc,
-                          acc[db][4 * rg + 2] * osc, acc[db][4 * rg + 3] * osc);
-            }
+            store_block_bf16(dst + db * 32, acc[db], osc, g, k_ok);
     };
 
     setup(it);

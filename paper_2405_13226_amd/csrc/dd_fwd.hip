@@ -84,7 +84,7 @@ __device__ __forceinline__ FwdItem fwd_item(int bid, int nqb, int B, int L, int 
 // dd_rope, so the result is bit-identical to a dd_rope pass) and, when
 // Qrot is not null, writes the rotated rows there for the backward.
 template <int D, bool PERSIST, bool ROPE>
-__global__ void __launch_bounds__(256, 2)
+__global__ void __launch_bounds__(256, D == 64 ? 3 : 2)
 fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
            const uint16_t *__restrict__ V, uint16_t *__restrict__ O, float *__restrict__ LSE,
            int B, int L, int H, int causal_i, const int32_t *__restrict__ cu, int n_docs,
@@ -290,21 +290,15 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
     // O = acc / l and the LSE of the current item.
     auto store = [&]() __attribute__((always_inline)) {
-        if (!q_ok)
-            return;
+        // Every lane takes part in the row sum's and the store's lane
+        // exchanges; lanes past L store nothing.
         const float l_tot = halves_sum(l_i);
         const float inv = 1.0f / l_tot;
-        uint16_t *Ob = O + it.base + my_q * rs;
+        uint16_t *Ob = O + it.base + static_cast<long long>(q_ok ? my_q : 0) * rs;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int rg = 0; rg < 4; ++rg) {
-                const int d = db * 32 + 8 * rg + 4 * g;
-                const bf16x4 v = pack4(acc[db][4 * rg] * inv, acc[db][4 * rg + 1] * inv,
-                                       acc[db][4 * rg + 2] * inv, acc[db][4 * rg + 3] * inv);
-                *reinterpret_cast<bf16x4 *>(Ob + d) = v;
-            }
-        if (g == 0)
+            store_block_bf16(Ob + db * 32, acc[db], inv, g, q_ok);
+        if (q_ok && g == 0)
             LSE[(static_cast<long long>(it.b) * L + my_q) * H + it.bh % H] =
                 (m_i + log2f(l_tot)) * kLn2;
     };
