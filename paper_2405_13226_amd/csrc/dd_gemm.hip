@@ -12,14 +12,17 @@
 // One workgroup (8 waves) computes a 256 x 256 tile of C; wave (wm, wn) owns
 // rows 128 wm .. +127 and columns 64 wn .. +63, i.e. 4 x 2 blocks of the
 // 32x32x16 bf16 product.  The K axis is walked in 64-wide steps: the A and B
-// tiles of a step are four 64 x 64 sub-tiles each, loaded into registers
-// (16 bytes per lane and sub-tile) during the previous step's products and
-// written to the other of two LDS stages after them, one barrier per step.
-// (Direct global->LDS loads would save the registers, but the compiler then
-// waits for them before every LDS read of the current step.)  An operand
-// stored with its reduction axis along the rows (A^T, B) is read with the
-// transposing LDS read; one stored with it along the columns is read
-// row-wise.  Both give a lane the 8 consecutive k of its row or column.
+// tiles of a step are four 64 x 64 sub-tiles each, in two LDS stages, one
+// barrier per step.  An operand stored with its reduction axis along the
+// rows (A^T, B) is read with the transposing LDS read; one stored with it
+// along the columns is read row-wise.  Both give a lane the 8 consecutive k
+// of its row or column.  When both operands are read row-wise (A, B^T: the
+// input gradients), the next step's sub-tiles arrive by direct global->LDS
+// loads of whole 128-byte rows into the attention kernels' swizzled
+// row-major layout, during the current step's products.  Otherwise they are
+// loaded into registers (16 bytes per lane and sub-tile) during the products
+// and written to the other stage after them: after a direct load the
+// compiler waits for it before every transposing LDS read.
 //
 // Each product is issued as D = op(B)^T op(A)^T, so a lane's accumulator holds
 // 4 consecutive columns of C in each register group: the epilogue writes 8
@@ -141,10 +144,20 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
     // Fragment i of A: rows (m) 32 i .. +31 of the wave's 128, sub-tile
     // 2 wm + i / 2; fragment j of B: columns 32 j .. +31 of the wave's 64,
     // sub-tile wn.  Sub-step kk: + SLAB kk (slabs) or + 16 rows.
+    // Direct loads (A and B^T): rows at tile_off<64>(row, 16 kk + 8 g); the
+    // swizzle depends on the row mod 16, so rows 32 further are 32 * 64
+    // elements further.
+    constexpr bool kDirect = !TA && TB;
+    int dro[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+        dro[kk] = tile_off<64>(l32, 16 * kk + 8 * g);
     auto a_frag = [&](const uint16_t *at, int i, int kk) __attribute__((always_inline)) {
         const uint16_t *sub = at + (2 * wm + (i >> 1)) * T::SUB;
         const int mo = 32 * (i & 1);
-        if constexpr (!TA)
+        if constexpr (kDirect)
+            return lds_row8(sub + mo * 64 + dro[kk]);
+        else if constexpr (!TA)
             return lds_row8(sub + kk * T::SLAB + row_off(mo));
         else
             return join(lds_tr4(sub + kk * 1024 + tr_off(mo, 0)),
@@ -153,7 +166,9 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
     auto b_frag = [&](const uint16_t *bt, int j, int kk) __attribute__((always_inline)) {
         const uint16_t *sub = bt + wn * T::SUB;
         const int no = 32 * j;
-        if constexpr (TB)
+        if constexpr (kDirect)
+            return lds_row8(sub + no * 64 + dro[kk]);
+        else if constexpr (TB)
             return lds_row8(sub + kk * T::SLAB + row_off(no));
         else
             return join(lds_tr4(sub + kk * 1024 + tr_off(no, 0)),
@@ -213,17 +228,47 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    load(0);
-    store(lds);
-    __syncthreads();
-    for (int kt = 0; kt < nkt; ++kt) {
-        const bool more = kt + 1 < nkt;
-        if (more)
-            load(kt + 1);
-        compute(lds + (kt & 1) * 2 * T::HALF);
-        if (more)
-            store(lds + ((kt + 1) & 1) * 2 * T::HALF);
+    if constexpr (kDirect) {
+        // Sub-tile s of A (B^T): rows 64 s .. +63 of the tile's rows (columns),
+        // the step's 64 k; one 1 KiB load instruction per wave and sub-tile.
+        DmaPlan<64, 64, T::NW> plan_a, plan_b;
+        plan_a.init(lda, wave, lane);
+        plan_b.init(ldb, wave, lane);
+        const uint16_t *ga = A + static_cast<long long>(m0) * lda + kbeg;
+        const uint16_t *gb = B + static_cast<long long>(n0) * ldb + kbeg;
+        constexpr int kNoClamp = 0x7fffffff;  // every tile lies inside the matrices
+        auto dma = [&](int kt, uint16_t *stage) __attribute__((always_inline)) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                plan_a.issue(stage + s * T::SUB, ga + kt * T::BK, lda, 64 * s, kNoClamp, wave,
+                             lane);
+                plan_b.issue(stage + T::HALF + s * T::SUB, gb + kt * T::BK, ldb, 64 * s,
+                             kNoClamp, wave, lane);
+            }
+        };
+        dma(0, lds);
+        wait_vmem();
         __syncthreads();
+        for (int kt = 0; kt < nkt; ++kt) {
+            if (kt + 1 < nkt)
+                dma(kt + 1, lds + ((kt + 1) & 1) * 2 * T::HALF);
+            compute(lds + (kt & 1) * 2 * T::HALF);
+            wait_vmem();
+            __syncthreads();
+        }
+    } else {
+        load(0);
+        store(lds);
+        __syncthreads();
+        for (int kt = 0; kt < nkt; ++kt) {
+            const bool more = kt + 1 < nkt;
+            if (more)
+                load(kt + 1);
+            compute(lds + (kt & 1) * 2 * T::HALF);
+            if (more)
+                store(lds + ((kt + 1) & 1) * 2 * T::HALF);
+            __syncthreads();
+        }
     }
 
     // Accumulator (i, j), register 4 q + e: column m = 32 i + l32 of the
