@@ -66,14 +66,20 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
     const int tiles_n = N / T::BN;
     // Workgroups are dispatched round-robin over the 8 XCDs (block id % 8),
     // each with its own L2.  Without a K split, XCD x takes the tile rows x,
-    // x + 8, ..., all tiles of a row one after another, so a row's A panel
-    // is fetched into one L2 and re-read from there (measured 2-7% faster
-    // than row-major tile order on the block's shapes).
+    // x + 8, ..., in bands of kGR of its rows; a band is walked in groups of
+    // kGC columns, each group column by column (kGR x kGC = 32 tiles, one
+    // per CU of the XCD), so the tiles that run at the same time share kGR
+    // A panels and kGC B panels in one L2.
     int tm, tn;
     if (gridDim.y == 1 && (M / T::BM) % kXcds == 0) {
+        constexpr int kGR = 4, kGC = 8;
         const int x = static_cast<int>(blockIdx.x) % kXcds, k = static_cast<int>(blockIdx.x) / kXcds;
-        tm = (k / tiles_n) * kXcds + x;
-        tn = k % tiles_n;
+        const int rows_x = (M / T::BM) / kXcds;
+        const int band = k / (kGR * tiles_n), rem = k % (kGR * tiles_n);
+        const int gr = min(kGR, rows_x - band * kGR);  // rows of this band
+        const int grp_c = rem / (gr * kGC), w = rem % (gr * kGC);
+        tm = (band * kGR + w % gr) * kXcds + x;
+        tn = grp_c * kGC + w / gr;
     } else {
         tm = static_cast<int>(blockIdx.x) / tiles_n;
         tn = static_cast<int>(blockIdx.x) % tiles_n;
