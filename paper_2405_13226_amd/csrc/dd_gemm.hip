@@ -13,13 +13,14 @@
 // rows 128 wm .. +127 and columns 64 wn .. +63, i.e. 4 x 2 blocks of the
 // 32x32x16 bf16 product.  The K axis is walked in 64-wide steps: the A and B
 // tiles of a step are four 64 x 64 sub-tiles each, in two LDS stages, one
-// barrier per step.  An operand stored with its reduction axis along the
-// rows (A^T, B) is read with the transposing LDS read; one stored with it
-// along the columns is read row-wise.  Both give a lane the 8 consecutive k
-// of its row or column.  When both operands are read row-wise (A, B^T: the
-// input gradients), the next step's sub-tiles arrive by direct global->LDS
-// loads of whole 128-byte rows into the attention kernels' swizzled
-// row-major layout, during the current step's products.  Otherwise they are
+// barrier per step.  Every sub-tile sits in LDS as the matrix stores it, in
+// the attention kernels' swizzled row-major layout.  An operand stored with
+// its reduction axis along the rows (A^T, B) is read with the transposing
+// LDS read; one stored with it along the columns is read row-wise.  Both
+// give a lane the 8 consecutive k of its row or column.  When both operands
+// are read row-wise (A, B^T: the input gradients), the next step's
+// sub-tiles arrive by direct global->LDS loads of whole 128-byte rows during
+// the current step's products.  Otherwise they are
 // loaded into registers (16 bytes per lane and sub-tile) during the products
 // and written to the other stage after them: after a direct load the
 // compiler waits for it before every transposing LDS read.
