@@ -78,7 +78,10 @@ __device__ __forceinline__ FwdItem fwd_item(int bid, int nqb, int B, int L, int 
 // PERSIST = false: one query block per workgroup.  PERSIST = true (short
 // rows): a workgroup walks its query blocks in the order of item_bid; during
 // a block's last key tile it DMAs the next block's first K/V tile into the
-// free stage, and after that tile loads the next block's Q rows.
+// free stage and (D = 64) the next block's Q rows into an LDS area of their
+// own, read into registers after that tile (at D = 128 the Q rows are loaded
+// from memory after the tile: the extra 32 KiB of LDS would cost a
+// workgroup per CU).
 // ROPE = true: Q holds the unrotated queries; each lane rotates its Q row
 // fragments right after loading them (positions and frequencies as
 // dd_rope, so the result is bit-identical to a dd_rope pass) and, when
@@ -93,7 +96,11 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     using T = FwdTile<D>;
     constexpr int KK = D / 16;  // k-steps of S^T
     constexpr int DB = D / 32;  // 32-row blocks of O^T
-    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE];
+    // Persistent D = 64: the next item's Q rows are staged here by direct
+    // loads during the current item's last tile (the register budget of
+    // three waves per SIMD has no room for a second set of Q fragments).
+    constexpr bool kQStage = PERSIST && D == 64;
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE + (kQStage ? T::BM * D : 0)];
 
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
@@ -131,13 +138,21 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     // query past L reads row L-1 instead (its scores are masked out and
     // nothing of it is stored).
     bf16x8 qf8[KK];
-    auto load_q = [&](const FwdItem &x) __attribute__((always_inline)) {
+    // from_lds: the rows were staged in LDS (kQStage), at the K-tile layout.
+    auto load_q = [&](const FwdItem &x, bool from_lds) __attribute__((always_inline)) {
         const int q_raw = x.qb * T::BM + wave * 32 + l32;
         const int q = min(q_raw, L - 1);
         const uint16_t *src = Q + x.base + q * rs + g * 8;
+        if (kQStage && from_lds) {
+            const uint16_t *qs = lds + 2 * T::STAGE + wave * 32 * D;
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-            qf8[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(src + kk * 16));
+            for (int kk = 0; kk < KK; ++kk)
+                qf8[kk] = lds_row8(qs + tile_off<D>(l32, kk * 16 + g * 8));
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk)
+                qf8[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(src + kk * 16));
+        }
         if constexpr (ROPE) {
             // Fragment kk holds dims kk*16 + 8g .. +7: pairs j = 8kk + 4g + e.
             // The opaque copies keep the frequency arithmetic here, once
@@ -311,7 +326,7 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     };
 
     setup(it);
-    load_q(it);
+    load_q(it, false);
     reset();
     int t = it.t_begin;
     issue(it, t, lds);
@@ -333,13 +348,26 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             if (more) {
                 nit = fwd_item<D>(nbid, nqb, B, L, H, causal, cu, n_docs);
                 issue(nit, nit.t_begin, other);
+                if constexpr (kQStage) {  // two 64-row halves with the tile plan
+                    plan.issue(lds + 2 * T::STAGE, Q + nit.base, rs, nit.qb * T::BM, L, wave,
+                               lane);
+                    plan.issue(lds + 2 * T::STAGE + T::BN * D, Q + nit.base, rs,
+                               nit.qb * T::BM + T::BN, L, wave, lane);
+                }
             }
         }
         compute(t, bufc);
-        if (more)  // Q of the next item (registers free after the tile)
-            load_q(nit);
+        if (!kQStage && more)  // Q of the next item (registers free after the tile)
+            load_q(nit, false);
         wait_vmem();
         __syncthreads();
+        if (kQStage && more) {  // the staged rows are in LDS
+            load_q(nit, true);
+            // Every wave has its rows before the next item's last tile
+            // stages the following rows (a one-tile item has no other
+            // barrier in between).
+            __syncthreads();
+        }
         if (!last) {
             ++t;
             return true;
