@@ -333,8 +333,9 @@ __device__ __forceinline__ QItem q_item(int bid, int nqb, int B, int L, int H, b
 // PERSIST = false: one query block per workgroup.  PERSIST = true (short
 // rows, D = 64 only; at D = 128 the item loop spills): a workgroup walks
 // its query blocks in the order of item_bid; during a block's last key tile
-// it DMAs the next block's first K/V tile into the free stage, and right
-// after that tile loads the next block's Q, dO and O rows.
+// it DMAs the next block's first K/V tile into the free stage and the next
+// block's Q and dO rows into LDS areas of their own (read into registers
+// after that tile), and loads its O rows and LSE into registers.
 template <int D, bool PERSIST>
 __global__ void __launch_bounds__(256, 2)
 dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
@@ -348,7 +349,11 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     using T = QTile<D>;
     constexpr int KK = D / 16;
     constexpr int DB = D / 32;
-    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE];
+    // Persistent (D = 64): the next item's Q and dO rows are staged here by
+    // direct loads during the current item's last tile, its O rows and LSE
+    // loaded into registers at the same time.
+    constexpr bool kRowStage = PERSIST;
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * T::STAGE + (kRowStage ? 2 * T::BM * D : 0)];
 
     const bool causal = causal_i != 0;
     const int tid = threadIdx.x;
@@ -390,7 +395,16 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     // row L-1 instead (its probabilities are masked to exactly 0 by a select
     // and nothing of it is stored).
     bf16x8 qf[KK], dof[KK], of[KK];
-    float neg_lse2 = 0.f, my_delta = 0.f;
+    float neg_lse2 = 0.f, my_delta = 0.f, lse_in = 0.f;
+    // O rows and the LSE of this lane's query (for delta and lse2).
+    auto load_o = [&](const QItem &x) __attribute__((always_inline)) {
+        const int qrow = min(x.qb * T::BM + wave * 32 + l32, L - 1);
+        const long long at = x.base + qrow * rs + g * 8;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+            of[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(O + at + kk * 16));
+        lse_in = LSE[(static_cast<long long>(x.b) * L + qrow) * H + x.bh % H];
+    };
     auto load_rows = [&](const QItem &x) __attribute__((always_inline)) {
         const int qrow = min(x.qb * T::BM + wave * 32 + l32, L - 1);
         const long long at = x.base + qrow * rs + g * 8;
@@ -398,11 +412,11 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         for (int kk = 0; kk < KK; ++kk) {
             qf[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(Q + at + kk * 16));
             dof[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(dO + at + kk * 16));
-            of[kk] = as_bf16x8(*reinterpret_cast<const u32x4 *>(O + at + kk * 16));
         }
+        load_o(x);
     };
     auto finish_rows = [&](const QItem &x) __attribute__((always_inline)) {
-        const int q = x.qb * T::BM + wave * 32 + l32, qrow = min(q, L - 1);
+        const int q = x.qb * T::BM + wave * 32 + l32;
         float part = 0.f;
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
@@ -410,8 +424,7 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             for (int i = 0; i < 8; ++i)
                 part += static_cast<float>(of[kk][i]) * static_cast<float>(dof[kk][i]);
         my_delta = part + __shfl_xor(part, 32);
-        const float lse2 =
-            LSE[(static_cast<long long>(x.b) * L + qrow) * H + x.bh % H] * kLog2e;
+        const float lse2 = lse_in * kLog2e;
         neg_lse2 = -lse2;
         if (q < L && g == 0) {
             const long long wrow = static_cast<long long>(x.bh) * L;
@@ -571,13 +584,36 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             if (more) {
                 nit = q_item<D>(nbid, nqb, B, L, H, causal, cu, n_docs);
                 issue(nit, nit.t_begin, other);
+                if constexpr (kRowStage) {  // 64-row halves with the tile plan
+                    uint16_t *rows = lds + 2 * T::STAGE;
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2) {
+                        const int r0 = nit.qb * T::BM + h2 * T::BN;
+                        plan.issue(rows + h2 * T::BN * D, Q + nit.base, rs, r0, L, wave, lane);
+                        plan.issue(rows + T::BM * D + h2 * T::BN * D, dO + nit.base, rs, r0, L,
+                                   wave, lane);
+                    }
+                    load_o(nit);  // registers free since the item's start
+                }
             }
         }
         compute(t, bufc);
-        if (more)  // Q, dO, O rows of the next item (registers free after the tile)
+        if (!kRowStage && more)  // Q, dO, O rows of the next item (registers free after the tile)
             load_rows(nit);
         wait_vmem();
         __syncthreads();
+        if (kRowStage && more) {  // the staged rows are in LDS
+            const uint16_t *rows = lds + 2 * T::STAGE + wave * 32 * D;
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                qf[kk] = lds_row8(rows + roff[kk]);
+                dof[kk] = lds_row8(rows + T::BM * D + roff[kk]);
+            }
+            // Every wave has its rows before the next item's last tile
+            // stages the following rows (a one-tile item has no other
+            // barrier in between).
+            __syncthreads();
+        }
         if (!last) {
             ++t;
             return true;
