@@ -145,6 +145,10 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const int qlo_r = qlo_k - i0 - 4 * g, qhi_r = qhi_k - i0 - 4 * g;
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
+            // A boundary tile's half whose queries none of the wave's keys
+            // sees adds nothing (its probabilities are all 0): skipped.
+            if (MASKED && (i0 + 32 * qb > hi_w || i0 + 32 * qb + 31 < lo_w))
+                continue;
             // dP accumulates onto -delta of its rows (C layout: register
             // 4*rg + e holds query 8*rg + 4*g + e), so the products give
             // dP - delta directly.
@@ -468,6 +472,10 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const int lo_r = lo_q - j0 - 4 * g, hi_r = hi_q - j0 - 4 * g;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
+            // A boundary tile's 32-key block that none of the wave's queries
+            // sees adds nothing (its probabilities are all 0): skipped.
+            if (MASKED && (j0 + 32 * kb > hi_w || j0 + 32 * kb + 31 < lo_w))
+                continue;
             // The A fragments are read in batches of KB_STEP k-steps before
             // their products, so several LDS reads are in flight at once
             // (two at D = 64, which keeps the kernel at 163 VGPRs, three

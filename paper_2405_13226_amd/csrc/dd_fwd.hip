@@ -15,7 +15,8 @@
 // row-major V tile (ds_read_b64_tr_b16).  The online softmax keeps a running max m and
 // sum l in fp32 (log2 domain), rescaling the O accumulator when m grows.
 // Key tiles entirely outside the mask are never visited; tiles entirely
-// inside it skip the element mask (only boundary tiles evaluate it).
+// inside it skip the element mask (only boundary tiles evaluate it), and in
+// a boundary tile a wave skips a 32-key block none of its queries sees.
 #include "dd_device.hpp"
 #include "dd_tile.hpp"
 #include "dd_internal.h"
@@ -217,14 +218,23 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         const uint16_t *kt = lds + BUF * T::STAGE;
         const uint16_t *vt = kt + T::TILE;
 
+        // A boundary tile's 32-key block that none of the wave's queries
+        // sees (scores all -inf, probabilities all 0) is skipped.
+        bool on[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+            on[kb] = !MASKED || !(j0 + 32 * kb > hi_w || j0 + 32 * kb + 31 < lo_w);
+
         // S^T = K Q^T for two 32-key blocks.
         f32x16 s[2];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             s[kb] = f32x16{};
+            if (on[kb]) {
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk)
-                s[kb] = mfma32(lds_row8(kt + kb * 32 * D + koff[kk]), qf8[kk], s[kb]);
+                for (int kk = 0; kk < KK; ++kk)
+                    s[kb] = mfma32(lds_row8(kt + kb * 32 * D + koff[kk]), qf8[kk], s[kb]);
+            }
         }
 
         // Boundary tiles: keys outside [lo_q, hi_q] -> -inf (branch-free).
@@ -263,13 +273,16 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
         float psum = 0.f;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb) {
+            if (on[kb]) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float p = fast_exp2(fmaf(s[kb][r], scale_log2, neg_m));
-                s[kb][r] = p;
-                psum += p;
+                for (int r = 0; r < 16; ++r) {
+                    const float p = fast_exp2(fmaf(s[kb][r], scale_log2, neg_m));
+                    s[kb][r] = p;
+                    psum += p;
+                }
             }
+        }
         l_i += psum;
 
         // O^T += V^T P^T.  B operand (kb, t2): registers 8*t2..8*t2+7 of
@@ -282,7 +295,9 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             for (int t2 = 0; t2 < 2; ++t2)
                 pb[kb][t2] = pack8(s[kb], 8 * t2);
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb) {
+            if (!on[kb])
+                continue;
 #pragma unroll
             for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
@@ -291,6 +306,7 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     const bf16x8 a = join(lds_tr4(vr + voff[db][0]), lds_tr4(vr + voff[db][1]));
                     acc[db] = mfma32(a, pb[kb][t2], acc[db]);
                 }
+        }
     };
 
     auto compute = [&](int t, auto bufc) {
