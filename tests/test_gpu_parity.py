@@ -94,6 +94,18 @@ def test_short_rows_persistent_several_slices(cuda, L, mode):
                tag=f"persistent one-kernel backward L={L} {mode}")
 
 
+# Persistent forward and dQ (D=64) whose items span a single key tile: rows
+# of at most 64 tokens, or a ragged last query block that starts a document
+# (documents of `doc` tokens).  Many items per workgroup, so the next item's
+# rows are staged in LDS while the current item's only tile runs.
+@pytest.mark.parametrize("B,L,H,doc", [(128, 48, 8, None), (64, 130, 8, 2), (16, 520, 8, 8)])
+def test_persistent_one_tile_items(cuda, B, L, H, doc):
+    cu = None if doc is None else dd.chunk_doclens([doc] * (B * L // doc), B * L)
+    bh = [(0, 0), (B // 2, H - 1), (B - 1, 3)]
+    check_case(B, L, H, 64, causal=True, cu=cu, seed=700 + L, bh=bh,
+               tag=f"persistent one-tile items B={B} L={L} doc={doc}")
+
+
 @pytest.mark.parametrize("B,L,D,causal", [(2, 700, 64, True), (2, 700, 128, False),
                                          (1, 2100, 64, True), (1, 2100, 128, True)])
 def test_large_scores_forward(cuda, B, L, D, causal):
