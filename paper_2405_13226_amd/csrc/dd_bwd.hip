@@ -470,6 +470,68 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
         // Blocks are processed one after the other so that only one block's
         // scores are live, which leaves registers for LDS reads in flight.
         const int lo_r = lo_q - j0 - 4 * g, hi_r = hi_q - j0 - 4 * g;
+        if constexpr (!MASKED && PERSIST) {
+            // Full tiles of the persistent form (two waves per SIMD anyway,
+            // its item loop holds more registers): both blocks' products at
+            // once (four independent accumulator chains), then both blocks'
+            // dS, then dQ.  In the other form the extra registers would cost
+            // the third wave per SIMD, which is worth more.
+            float nd = -my_delta;
+            asm volatile("" : "+v"(nd));
+            f32x16 s2[2], dp2[2];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                s2[kb] = f32x16{};
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    dp2[kb][r] = nd;
+            }
+#pragma unroll
+            for (int k0 = 0; k0 < KK; k0 += 2) {
+                bf16x8 ka[2][2], va[2][2];
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) {
+                        const int off = kb * 32 * D + roff[k0 + i];
+                        ka[kb][i] = lds_row8(ks + off);
+                        va[kb][i] = lds_row8(vs + off);
+                    }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb) {
+                        s2[kb] = mfma32(ka[kb][i], qf[k0 + i], s2[kb]);
+                        dp2[kb] = mfma32(va[kb][i], dof[k0 + i], dp2[kb]);
+                    }
+            }
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    dp2[kb][r] = fast_exp2(fmaf(s2[kb][r], scale_log2, neg_lse2)) * dp2[kb][r];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                bf16x8 kt[2][DB];
+#pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+                    for (int db = 0; db < DB; ++db) {
+                        const uint16_t *kr = ks + (kb * 32 + 16 * t2) * D;
+                        kt[t2][db] = join(lds_tr4(kr + toff[db][0]), lds_tr4(kr + toff[db][1]));
+                    }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2) {
+                    const bf16x8 sb = pack8(dp2[kb], 8 * t2);
+#pragma unroll
+                    for (int db = 0; db < DB; ++db)
+                        dq[db] = mfma32(kt[t2][db], sb, dq[db]);
+                }
+            }
+            return;
+        }
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             // A boundary tile's 32-key block that none of the wave's queries
