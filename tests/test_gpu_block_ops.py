@@ -33,6 +33,9 @@ def f64(t):
 @pytest.mark.parametrize("M,N,K,ta,tb", [
     (256, 256, 64, 0, 0), (512, 768, 320, 0, 1), (768, 512, 192, 1, 0),
     (1024, 512, 8192, 1, 0),      # long K: split over several workgroups
+    # 40 tile rows (5 per XCD: a band of 4 rows and one of 1) and 11 tile
+    # columns (column groups of 8 and 3) in the grouped tile order
+    (10240, 2816, 128, 0, 0), (10240, 2816, 128, 0, 1),
     (65536, 2048, 2048, 0, 0),    # the block's output projection at 65,536 tokens
     (2048, 2048, 65536, 1, 0),    # its weight gradient
 ])
