@@ -194,10 +194,7 @@ gemm_kernel(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, uint
         }
         // reads per K step: A 16 row reads or 32 transposed halves, B 8 row
         // reads or 16 transposed halves
-#ifndef GEMM_AHEAD
-#define GEMM_AHEAD 8
-#endif
-        constexpr int kAhead = GEMM_AHEAD;
+        constexpr int kAhead = 8;
         constexpr int NR = (TA ? 32 : 16) + (TB ? 8 : 16);
         constexpr int NP = 32;
         constexpr int QR = (NR - kAhead) / NP, RR = (NR - kAhead) % NP;
