@@ -604,8 +604,8 @@ def main():
 
 
 def run_layer(args, buckets, dev):
-    """One OpenLM-1B block fwd+bwd per bucket (torch autograd; attention and RoPE
-    in the library's kernels, projections and MLP as vendor GEMMs)."""
+    """One OpenLM-1B block fwd+bwd per bucket (one autograd node; every step in
+    the library's kernels: GEMMs, LayerNorms, SwiGLU, RoPE and attention)."""
     import numpy as np
     import torch
     from paper_2405_13226_amd import _lib, dd
@@ -686,9 +686,10 @@ def run_gemm(args, dev):
     from paper_2405_13226_amd.layer import OPENLM_1B
 
     T, d, hid = TOKENS, OPENLM_1B["d"], OPENLM_1B["hidden"]
-    # (name, M, N, K, trans_a, trans_b): y = x W, dx = dy W^T, dW = x^T dy
-    shapes = [("qkv fwd", T, 3 * d, d, 0, 0), ("out fwd", T, d, d, 0, 0),
-              ("w1 fwd", T, hid, d, 0, 0), ("w2 fwd", T, d, hid, 0, 0),
+    # (name, M, N, K, trans_a, trans_b): y = x (W^T)^T (the block's forward
+    # reads transposed weight copies), dx = dy W^T, dW = x^T dy
+    shapes = [("qkv fwd", T, 3 * d, d, 0, 1), ("out fwd", T, d, d, 0, 1),
+              ("w1 fwd", T, hid, d, 0, 1), ("w2 fwd", T, d, hid, 0, 1),
               ("qkv dx", T, d, 3 * d, 0, 1), ("w1 dx", T, d, hid, 0, 1),
               ("w2 dx", T, hid, d, 0, 1), ("qkv dW", d, 3 * d, T, 1, 0),
               ("w1 dW", d, hid, T, 1, 0), ("w2 dW", hid, d, T, 1, 0)]

@@ -238,6 +238,18 @@ int dd_swiglu_fwd(const void *U, const void *V, void *Y, long long n, void *stre
 int dd_swiglu_bwd(const void *U, const void *V, const void *dY, void *dU, void *dV, long long n,
                   void *stream);
 
+/*
+ * Y = X^T for a bf16 matrix X [rows, cols] (row stride ldx): Y [cols, rows]
+ * (row stride ldy), Y[c][r] = X[r][c], bit-exact.  The block's forward
+ * products read their weights through it (Sec. 3.1; Table "openlm1b": the
+ * d x 3d, d x d, d x 5632 and 5632 x d projections), so that both operands
+ * of every forward product are read row-wise.  rows, cols: multiples of 64,
+ * rows * cols <= 2^36; ldx >= cols, ldy >= rows, both multiples of 8;
+ * pointers 16-byte aligned; X and Y must not overlap.
+ */
+int dd_transpose(const void *X, long long ldx, void *Y, long long ldy, int rows, int cols,
+                 void *stream);
+
 /* Workspace bytes dd_attn_bwd needs for this shape (0 for an invalid shape). */
 size_t dd_attn_bwd_workspace_bytes(int B, int L, int H, int D);
 

@@ -33,6 +33,7 @@ SIGNATURES = {
                                         ctypes.c_size_t, _P]),
     "dd_layernorm_bwd_workspace_bytes": (ctypes.c_size_t, [_I, _I]),
     "dd_swiglu_fwd": (ctypes.c_int, [_P, _P, _P, ctypes.c_longlong, _P]),
+    "dd_transpose": (ctypes.c_int, [_P, ctypes.c_longlong, _P, ctypes.c_longlong, _I, _I, _P]),
     "dd_swiglu_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_longlong, _P]),
     "dd_doclens_check": (ctypes.c_int, [_P, _I, ctypes.c_longlong]),
     "dd_status_str": (ctypes.c_char_p, [_I]),

@@ -64,6 +64,21 @@ def gemm(a, b, trans_a: bool = False, trans_b: bool = False, residual=None, out=
     return out
 
 
+def transpose(x, out=None):
+    """x.T as a bf16 matrix with unit column stride (into ``out`` if given)."""
+    _mat(x, "x")
+    R, C = x.shape
+    if out is None:
+        out = torch.empty((C, R), dtype=torch.bfloat16, device=x.device)
+    _mat(out, "out")
+    if tuple(out.shape) != (C, R):
+        raise ValueError(f"out has shape {tuple(out.shape)}, expected {(C, R)}")
+    st = lib().dd_transpose(_p(x), x.stride(0), _p(out), out.stride(0), R, C,
+                            _stream(x.device))
+    check(st, "dd_transpose")
+    return out
+
+
 def layer_norm(x, w, b, eps: float = LN_EPS):
     """(y, mean, rstd) of LayerNorm over the rows of x [rows, d]."""
     _mat(x, "x")

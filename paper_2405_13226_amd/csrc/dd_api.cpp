@@ -461,6 +461,24 @@ int dd_swiglu_bwd(const void *U, const void *V, const void *dY, void *dU, void *
     return dd::launch_swiglu(a);
 }
 
+int dd_transpose(const void *X, long long ldx, void *Y, long long ldy, int rows, int cols,
+                 void *stream)
+{
+    if (!X || !Y)
+        return DD_ERR_NULL;
+    if (rows < 64 || cols < 64 || rows % 64 || cols % 64 ||
+        static_cast<long long>(rows) * cols > (1LL << 36) || ldx < cols || ldy < rows)
+        return DD_ERR_SHAPE;
+    if (ldx % 8 || ldy % 8 || !aligned(X, 16) || !aligned(Y, 16))
+        return DD_ERR_ALIGN;
+    Range rx = range_of(X, static_cast<size_t>((static_cast<long long>(rows) - 1) * ldx + cols) * 2);
+    Range ry = range_of(Y, static_cast<size_t>((static_cast<long long>(cols) - 1) * ldy + rows) * 2);
+    if (overlaps(rx, ry))
+        return DD_ERR_ALIAS;
+    dd::TransposeArgs a{X, Y, ldx, ldy, rows, cols, stream};
+    return dd::launch_transpose(a);
+}
+
 int dd_rope(const void *X, void *Y, int B, int L, int H, int D, float base, int inverse,
             const int32_t *cu_doclens, int n_docs, int doc_positions, void *stream)
 {

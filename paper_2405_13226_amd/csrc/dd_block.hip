@@ -351,6 +351,49 @@ int launch_layernorm_bwd(const LayerNormArgs &a)
     return e == hipSuccess ? DD_OK : DD_ERR_HIP;
 }
 
+// Y[c][r] = X[r][c] for a bf16 matrix, one 64 x 64 tile per workgroup:
+// 16-byte row pieces of X into LDS (rows padded by 16 bytes), then each
+// thread gathers eight elements of a tile column and writes them as a
+// 16-byte piece of a Y row.
+__global__ void __launch_bounds__(256)
+transpose_kernel(const uint16_t *__restrict__ X, uint16_t *__restrict__ Y, int tiles_c,
+                 long long ldx, long long ldy)
+{
+    constexpr int P = 72;  // LDS row pitch (elements)
+    __shared__ __attribute__((aligned(16))) uint16_t t[64 * P];
+    const int tid = threadIdx.x;
+    const long long r0 = static_cast<long long>(blockIdx.x / tiles_c) * 64;
+    const long long c0 = static_cast<long long>(blockIdx.x % tiles_c) * 64;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int q = tid + 256 * i, r = q >> 3, c = (q & 7) * 8;
+        *reinterpret_cast<u32x4 *>(t + r * P + c) =
+            *reinterpret_cast<const u32x4 *>(X + (r0 + r) * ldx + c0 + c);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int q = tid + 256 * i, j = q >> 3, k = (q & 7) * 8;  // Y row c0 + j, columns r0 + k ..
+        u32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            w[e] = static_cast<uint32_t>(t[(k + 2 * e) * P + j]) |
+                   (static_cast<uint32_t>(t[(k + 2 * e + 1) * P + j]) << 16);
+        *reinterpret_cast<u32x4 *>(Y + (c0 + j) * ldy + r0 + k) = w;
+    }
+}
+
+int launch_transpose(const TransposeArgs &a)
+{
+    const int tiles_c = a.cols / 64;
+    const long long tiles = static_cast<long long>(a.rows / 64) * tiles_c;
+    const hipError_t e = launch_kernel(transpose_kernel, dim3(static_cast<unsigned>(tiles)),
+                                       dim3(256), static_cast<hipStream_t>(a.stream),
+                                       static_cast<const uint16_t *>(a.X),
+                                       static_cast<uint16_t *>(a.Y), tiles_c, a.ldx, a.ldy);
+    return e == hipSuccess ? DD_OK : DD_ERR_HIP;
+}
+
 int launch_swiglu(const SwigluArgs &a)
 {
     hipStream_t st = static_cast<hipStream_t>(a.stream);

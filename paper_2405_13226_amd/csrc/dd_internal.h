@@ -107,6 +107,17 @@ struct SwigluArgs {
 };
 int launch_swiglu(const SwigluArgs &a);
 
+// Y [cols, rows] = X [rows, cols] transposed (bf16, rows and cols multiples
+// of 64, row strides in elements).
+struct TransposeArgs {
+    const void *X;
+    void *Y;
+    long long ldx, ldy;
+    int rows, cols;
+    void *stream;
+};
+int launch_transpose(const TransposeArgs &a);
+
 // Both return a dd_status value (DD_OK or DD_ERR_HIP).
 int launch_fwd(const FwdArgs &a);
 int launch_bwd(const BwdArgs &a);

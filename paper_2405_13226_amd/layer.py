@@ -13,7 +13,10 @@ embeddings):
 LayerNorms have weight and bias, projections have none, the SwiGLU width is
 5632 at d = 2048.  Every step runs in this library's HIP kernels: the
 projections and the MLP products in its bf16 GEMM (the residual additions in
-the GEMM epilogue), the LayerNorms and the SwiGLU in its elementwise kernels,
+the GEMM epilogue; the forward multiplies by transposed copies of the weights,
+made by its transpose kernel at the start of the step, so that both operands
+of every forward product are read along rows, the GEMM's faster form), the
+LayerNorms and the SwiGLU in its elementwise kernels,
 RoPE and attention in the attention kernels; the backward is written out
 step by step (one autograd node for the whole block).  The block exists to
 place the attention hot path in a full layer step: its time as a share of
@@ -40,16 +43,20 @@ class _BlockFunction(torch.autograd.Function):
                 docs, doc_pos):
         B, L, H, D = shape
         d = H * D
+        # transposed weight copies: every forward product then reads both of
+        # its operands along rows (the GEMM's faster operand form)
+        t_qkv, t_o, t_1, t_3, t_2 = (ops.transpose(w) for w in (w_qkv, w_o, w_1, w_3, w_2))
         a, mean1, rstd1 = ops.layer_norm(x, ln1_w, ln1_b, LN_EPS)
-        q, k, v = (ops.gemm(a, w_qkv[:, i * d:(i + 1) * d]) for i in range(3))
+        q, k, v = (ops.gemm(a, t_qkv[i * d:(i + 1) * d], trans_b=True) for i in range(3))
         o, lse, qr, kr = forward_rope(q.view(B, L, H, D), k.view(B, L, H, D),
                                       v.view(B, L, H, D), base, True, docs, doc_pos)
         o2 = o.view(B * L, d)
-        h = ops.gemm(o2, w_o, residual=x)
+        h = ops.gemm(o2, t_o, trans_b=True, residual=x)
         m, mean2, rstd2 = ops.layer_norm(h, ln2_w, ln2_b, LN_EPS)
-        u1, u3 = ops.gemm(m, w_1), ops.gemm(m, w_3)
+        u1, u3 = ops.gemm(m, t_1, trans_b=True), ops.gemm(m, t_3, trans_b=True)
         g = ops.swiglu(u1, u3)
-        y = ops.gemm(g, w_2, residual=h)
+        y = ops.gemm(g, t_2, trans_b=True, residual=h)
+        del t_qkv, t_o, t_1, t_3, t_2
         ctx.save_for_backward(x, ln1_w, w_qkv, w_o, ln2_w, w_1, w_3, w_2, a, mean1, rstd1, qr,
                               kr, v, o, lse, h, m, mean2, rstd2, u1, u3, g)
         ctx.cfg = (shape, base, docs, doc_pos)

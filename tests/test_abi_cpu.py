@@ -239,6 +239,16 @@ def test_block_kernel_validation(lib):
     assert lib.dd_swiglu_fwd(fake(0), fake(1), fake(2), 12, None) == SHAPE
     assert lib.dd_swiglu_fwd(fake(0), fake(1), fake(0, 16), 64, None) == ALIAS
     assert lib.dd_swiglu_bwd(fake(0), fake(1), fake(2), fake(3), fake(3, 16), 64, None) == ALIAS
+    # transpose
+    tr = lambda **kw: lib.dd_transpose(kw.get("X", fake(0)), kw.get("ldx", 192),
+                                       kw.get("Y", fake(1)), kw.get("ldy", 128),
+                                       kw.get("rows", 128), kw.get("cols", 192), None)
+    assert tr(X=None) == NULL and tr(Y=None) == NULL
+    for kw in (dict(rows=0), dict(rows=96), dict(cols=100), dict(ldx=128), dict(ldy=64),
+               dict(rows=1 << 19, cols=1 << 18, ldx=1 << 18, ldy=1 << 19)):
+        assert tr(**kw) == SHAPE, kw
+    assert tr(ldx=196) == ALIGN and tr(X=fake(0, 8)) == ALIGN
+    assert tr(Y=fake(0, 1024)) == ALIAS
 
 
 def test_noalloc_backward_validation(lib):

@@ -108,6 +108,19 @@ def test_layer_norm(cuda, rows, d):
     assert res["mean"] <= 1e-5 and res["rstd"] <= 1e-5
 
 
+@pytest.mark.parametrize("R,C,pad", [(64, 64, 0), (192, 320, 0), (2048, 5632, 0),
+                                     (5632, 2048, 64)])
+def test_transpose(cuda, R, C, pad):
+    # bit-exact against the transposed copy; pad > 0: strided views in and out
+    x = bf16((R, C + pad), 7)
+    xd = x.to(cuda)[:, pad // 2:pad // 2 + C]
+    y = torch.empty((C, R + 2 * pad), dtype=torch.bfloat16, device=cuda)[:, :R]
+    ops.transpose(xd, out=y)
+    torch.cuda.synchronize()
+    ref = x[:, pad // 2:pad // 2 + C].view(torch.int16).numpy().T
+    assert np.array_equal(y.cpu().view(torch.int16).numpy(), ref)
+
+
 def test_swiglu(cuda):
     n = 3 * 1024 * 8 + 64
     u, v, dy = bf16((n,), 1, 3.0), bf16((n,), 2), bf16((n,), 3)
