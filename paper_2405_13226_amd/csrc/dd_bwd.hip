@@ -132,7 +132,7 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     }
 
     f32x16 dk[DB], dv[DB];
-    DmaPlan<D, T::BM, T::NW> plan;
+    DmaPlan<D, T::BM, T::NW, true> plan;
     plan.init(rs, wave, lane);
 
     auto body = [&](int i0, auto bufc, auto maskc) {

@@ -133,7 +133,7 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
     f32x16 acc[DB];  // dV^T (role A) or dK^T (role B)
 
-    DmaPlan<D, T::BM, T::NW> plan;
+    DmaPlan<D, T::BM, T::NW, !PERSIST> plan;
     plan.init(rs, wave, lane);
 
     // Transposed A operand (rows of the 16-query step of (qb, t2)) times a

@@ -44,6 +44,49 @@ __device__ __forceinline__ lds_void *to_lds(const void *p)
     return (lds_void *)(p);
 }
 
+// Direct global->LDS loads through inline assembly (DmaPlan<..., true> and
+// dma_row_f32<true>).  Lane i's SIZE bytes from `g` land at LDS byte address
+// m0 + i * SIZE, with m0 the wave-uniform `lds_base`.  Issued through the
+// builtin instead, the loads make the compiler wait for all of them (vmcnt(0))
+// before every later ds_read_b64_tr_b16 of the wave, whatever LDS it reads:
+// in a double-buffered tile loop that is a wait for the next tile's prefetch
+// in the middle of the current tile.  The compiler does not know what the
+// assembly writes, so every tile is read only after the wait_vmem() and the
+// workgroup barrier that follow its loads (as all callers do).  The assembly
+// also orders every other memory access of the kernel around it, which costs
+// registers in some kernels: each kernel takes the form measured faster.
+__device__ __forceinline__ uint32_t lds_base_sgpr(const void *p)
+{
+    const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(to_lds(p)));
+    return __builtin_amdgcn_readfirstlane(a);
+}
+
+__device__ __forceinline__ void dma_b128(const void *g, uint32_t lds_base)
+{
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(lds_base), "v"(g)
+                 : "m0", "memory");
+}
+
+// The same with a wave-uniform base address and a 32-bit per-lane byte
+// offset (no 64-bit address arithmetic per load).
+__device__ __forceinline__ void dma_b128_off(const void *base, uint32_t off, uint32_t lds_base)
+{
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(lds_base), "v"(off), "s"(base)
+                 : "m0", "memory");
+}
+
+__device__ __forceinline__ void dma_b32(const void *g, uint32_t lds_base)
+{
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
+                 :
+                 : "s"(lds_base), "v"(g)
+                 : "m0", "memory");
+}
+
 // Direct-to-LDS loads of one tile.  Every wave of the workgroup (NW waves)
 // takes a share of the 64-slot (1 KiB) load instructions; slot q of the tile
 // holds row q / (D/8), stored chunk q % (D/8).  The byte offsets of a wave's
@@ -51,7 +94,7 @@ __device__ __forceinline__ lds_void *to_lds(const void *p)
 // that runs past row L-1 takes a slow path that clamps rows to L-1 (their
 // values are finite and the mask removes them).  Completion is tracked by
 // vmcnt.
-template <int D, int ROWS, int NW>
+template <int D, int ROWS, int NW, bool ASM = false>
 struct DmaPlan {
     static constexpr int CPR = D / 8;               // chunks per row
     static constexpr int INSTRS = ROWS * CPR / 64;  // wave instructions per tile
@@ -75,17 +118,26 @@ struct DmaPlan {
         if (row0 + ROWS <= L) {
             const char *gb = reinterpret_cast<const char *>(g + row0 * rs);
 #pragma unroll
-            for (int k = 0; k < PER; ++k)
-                __builtin_amdgcn_global_load_lds(gb + off[k], to_lds(lds_tile + (wave + NW * k) * 512),
-                                                 16, 0, 0);
+            for (int k = 0; k < PER; ++k) {
+                if constexpr (ASM)
+                    dma_b128_off(gb, off[k], lds_base_sgpr(lds_tile + (wave + NW * k) * 512));
+                else
+                    __builtin_amdgcn_global_load_lds(gb + off[k],
+                                                     to_lds(lds_tile + (wave + NW * k) * 512), 16,
+                                                     0, 0);
+            }
         } else {
 #pragma unroll
             for (int k = 0; k < PER; ++k) {
                 const int q = (wave + NW * k) * 64 + lane;
                 const int r = q / CPR, x = (q % CPR) ^ swz<D>(r);
                 const int row = min(row0 + r, L - 1);
-                __builtin_amdgcn_global_load_lds(g + row * rs + x * 8,
-                                                 to_lds(lds_tile + (wave + NW * k) * 512), 16, 0, 0);
+                if constexpr (ASM)
+                    dma_b128(g + row * rs + x * 8, lds_base_sgpr(lds_tile + (wave + NW * k) * 512));
+                else
+                    __builtin_amdgcn_global_load_lds(g + row * rs + x * 8,
+                                                     to_lds(lds_tile + (wave + NW * k) * 512), 16,
+                                                     0, 0);
             }
         }
     }
@@ -93,11 +145,15 @@ struct DmaPlan {
 
 // Direct-to-LDS load of ROWS consecutive fp32 values (ROWS == 64: one wave
 // instruction of 4-byte slots), rows clamped to L-1.
+template <bool ASM>
 __device__ __forceinline__ void dma_row_f32(float *lds, const float *__restrict__ g, int row0,
                                             int L, int lane)
 {
     const int row = min(row0 + lane, L - 1);
-    __builtin_amdgcn_global_load_lds(g + row, to_lds(lds), 4, 0, 0);
+    if constexpr (ASM)
+        dma_b32(g + row, lds_base_sgpr(lds));
+    else
+        __builtin_amdgcn_global_load_lds(g + row, to_lds(lds), 4, 0, 0);
 }
 
 // Wait for this wave's outstanding vector-memory operations (incl. LDS DMA).
