@@ -190,6 +190,8 @@ def parse():
                          "traffic that scales FETCH_SIZE / WRITE_SIZE counter runs)")
     ap.add_argument("--no-extras", action="store_true",
                     help="default run only: skip the D=128 sweep and chunk_vs_dd extras")
+    ap.add_argument("--sq-summary", nargs=2, metavar=("PASS1_DIR", "PASS2_DIR"),
+                    help="print the SQ counter table of two rocprofv3 counter runs and exit")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 counter runs of this script (no GPU use)")
     return ap.parse_args()
@@ -556,6 +558,8 @@ def main():
     args = parse()
     if args.traffic_summary:
         return traffic_summary(args)
+    if args.sq_summary:
+        return sq_summary(args)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): every (b, h) slice "
               "of the attention path is independent, so there is no cross-GPU exchange to "
@@ -914,6 +918,82 @@ def traffic_summary(args):
         lines.append(f"fetch_bytes_per_launch.{kname}.{gname} = {int(v['fetch'])}")
         lines.append(f"write_bytes_per_launch.{kname}.{gname} = {int(v['write'])}")
         lines.append(f"bytes_per_launch.{kname}.{gname} = {int(v['fetch'] + v['write'])}")
+    print("\n".join(lines))
+
+
+def sq_summary(args):
+    """Markdown table (stdout) of SQ counters per (group, kernel) of the last
+    bench step, from two rocprofv3 counter runs of this script (pass 1:
+    SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_WAVE_CYCLES
+    SQ_WAIT_ANY SQ_WAIT_INST_ANY ... GRBM_GUI_ACTIVE; pass 2: SQ_WAIT_INST_LDS
+    SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_LDS ... GRBM_GUI_ACTIVE), each with
+    --steps 1 --warmup 1.  GRBM_GUI_ACTIVE is summed over the 8 XCDs; the
+    matrix-pipe shares are over (GUI / 8) * 1024 SIMD-cycles, the wait shares
+    over SQ_WAVE_CYCLES."""
+    import csv
+    import glob
+    import re
+
+    fam = {"fwd_kernel": "forward", "dq_kernel": "backward_dq", "dkdv1_kernel": "backward_dkdv",
+           "dkdv_kernel": "backward_dkdv", "bwd_short_kernel": "backward_short",
+           "bwd_short_persist_kernel": "backward_short", "rope_kernel": "rope"}
+    kid = {"forward": 0, "rope": 4, "backward_dq": 3, "backward_dkdv": 2, "backward_short": 1}
+
+    def read(d):
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not f:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        disp = {}
+        for r in csv.DictReader(open(f[0])):
+            m = re.search(r"dd::(\w+)(<[^>]*>)?", r["Kernel_Name"])
+            if not m or m.group(1) not in fam:
+                continue
+            did = int(r["Dispatch_Id"])
+            e = disp.setdefault(did, {"kernel": m.group(1) + (m.group(2) or ""),
+                                      "fam": fam[m.group(1)],
+                                      "ms": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6})
+            e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        return [disp[k] for k in sorted(disp)]
+
+    groups, desc = workload(args.workload, args.seed,
+                            [int(x) for x in args.buckets.split(",")] if args.buckets else None)
+    passes = []
+    for d in args.sq_summary:
+        rows = read(d)
+        names = [r["fam"] for r in rows]
+        fwd_idx = [i for i, n in enumerate(names) if n == "forward"]
+        if len(fwd_idx) < len(groups):
+            raise SystemExit("fewer forward launches than groups")
+        start = fwd_idx[-len(groups)]
+        while start > 0 and names[start - 1] == "rope":
+            start -= 1
+        passes.append(rows[start:])
+    if len(passes[0]) != len(passes[1]):
+        raise SystemExit("the two passes hold different launch sequences")
+    merged = []
+    for a, b in zip(*passes):
+        if a["kernel"] != b["kernel"]:
+            raise SystemExit("the two passes hold different launch sequences")
+        merged.append({**b, **a})
+    nm = {v: k for k, v in kid.items()}
+    by = split_by_group([(kid[m["fam"]], m) for m in merged], nm, len(groups))
+    lines = ["| L | kernel | ms | SCLK GHz | MFMA busy % | MFMA+VALU co-issue % | waves waiting % "
+             "| waiting to issue % | waiting on LDS issue % | VALU / MFMA instr | LDS / MFMA instr |",
+             "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for g, kl in zip(groups, by):
+        for fname in ("rope", "forward", "backward_short", "backward_dq", "backward_dkdv"):
+            for m in kl.get(fname, []):
+                gui = m["GRBM_GUI_ACTIVE"] / 8.0
+                simd = gui * 1024.0
+                wave = m["SQ_WAVE_CYCLES"]
+                mf = max(m["SQ_INSTS_MFMA"], 1.0)
+                lines.append(
+                    f"| {g['L']} | `{m['kernel']}` | {m['ms']:.3f} | {gui / (m['ms'] * 1e-3) / 1e9:.2f} "
+                    f"| {100 * m['SQ_VALU_MFMA_BUSY_CYCLES'] / simd:.0f} "
+                    f"| {100 * m['SQ_VALU_MFMA_COEXEC_CYCLES'] / simd:.0f} "
+                    f"| {100 * m['SQ_WAIT_ANY'] / wave:.0f} | {100 * m['SQ_WAIT_INST_ANY'] / wave:.0f} "
+                    f"| {100 * m['SQ_WAIT_INST_LDS'] / wave:.0f} "
+                    f"| {m['SQ_INSTS_VALU'] / mf:.1f} | {m['SQ_INSTS_LDS'] / mf:.2f} |")
     print("\n".join(lines))
 
 
