@@ -132,7 +132,8 @@ dkdv1_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     }
 
     f32x16 dk[DB], dv[DB];
-    DmaPlan<D, T::BM, T::NW, true> plan;
+    // kDmaAsm lets the compiler spill the one-block form (28 VGPRs).
+    DmaPlan<D, T::BM, T::NW, kDmaAsmCast> plan;
     plan.init(rs, wave, lane);
 
     auto body = [&](int i0, auto bufc, auto maskc) {
@@ -451,7 +452,7 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     }
 
     f32x16 dq[DB];
-    DmaPlan<D, T::BN, 4> plan;
+    DmaPlan<D, T::BN, 4, kDmaAsm> plan;
     plan.init(rs, wave, lane);
     auto issue = [&](const QItem &x, int t, uint16_t *stage) __attribute__((always_inline)) {
         plan.issue(stage, K + x.base, rs, t * T::BN, L, wave, lane);

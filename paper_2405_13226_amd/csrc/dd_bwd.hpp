@@ -72,8 +72,8 @@ __device__ __forceinline__ KvItem kv_item(int bid, int nkb, int B, int L, int H,
 // Direct-to-LDS loads of query tile t of item x into `stage`: the Q and dO
 // tiles (T::TILE elements each), then lse2 and -delta of its rows (waves 0
 // and 1).
-template <int D, class T, bool ASM>
-__device__ __forceinline__ void kv_issue(const DmaPlan<D, T::BM, T::NW, ASM> &plan, uint16_t *stage,
+template <int D, class T, int MODE>
+__device__ __forceinline__ void kv_issue(const DmaPlan<D, T::BM, T::NW, MODE> &plan, uint16_t *stage,
                                          const uint16_t *__restrict__ Q,
                                          const uint16_t *__restrict__ dO,
                                          const float *__restrict__ lse2g,
@@ -85,9 +85,9 @@ __device__ __forceinline__ void kv_issue(const DmaPlan<D, T::BM, T::NW, ASM> &pl
     plan.issue(stage + T::TILE, dO + x.base, rs, i0, L, wave, lane);
     float *fs = reinterpret_cast<float *>(stage + 2 * T::TILE);
     if (wave == 0)
-        dma_row_f32<ASM>(fs, lse2g + static_cast<long long>(x.bh) * L, i0, L, lane);
+        dma_row_f32<MODE>(fs, lse2g + static_cast<long long>(x.bh) * L, i0, L, lane);
     else if (wave == 1)
-        dma_row_f32<ASM>(fs + T::BM, ndeltag + static_cast<long long>(x.bh) * L, i0, L, lane);
+        dma_row_f32<MODE>(fs + T::BM, ndeltag + static_cast<long long>(x.bh) * L, i0, L, lane);
 }
 
 

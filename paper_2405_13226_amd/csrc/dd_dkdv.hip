@@ -133,7 +133,9 @@ dkdv_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
 
     f32x16 acc[DB];  // dV^T (role A) or dK^T (role B)
 
-    DmaPlan<D, T::BM, T::NW, !PERSIST> plan;
+    // Tile loads through assembly in the one-block form; the persistent
+    // form measured faster with the builtin at L = 512 and 1024.
+    DmaPlan<D, T::BM, T::NW, PERSIST ? kDmaBuiltin : kDmaAsm> plan;
     plan.init(rs, wave, lane);
 
     // Transposed A operand (rows of the 16-query step of (qb, t2)) times a

@@ -204,7 +204,7 @@ fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
     f32x16 acc[DB];
     float m_i = -INFINITY, l_i = 0.f;
 
-    DmaPlan<D, T::BN, 4, D == 64 && !PERSIST> plan;
+    DmaPlan<D, T::BN, 4, kDmaAsm> plan;
     plan.init(rs, wave, lane);
     auto issue = [&](const FwdItem &x, int t, uint16_t *stage) __attribute__((always_inline)) {
         plan.issue(stage, K + x.base, rs, t * T::BN, L, wave, lane);

@@ -44,21 +44,36 @@ __device__ __forceinline__ lds_void *to_lds(const void *p)
     return (lds_void *)(p);
 }
 
-// Direct global->LDS loads through inline assembly (DmaPlan<..., true> and
-// dma_row_f32<true>).  Lane i's SIZE bytes from `g` land at LDS byte address
-// m0 + i * SIZE, with m0 the wave-uniform `lds_base`.  Issued through the
-// builtin instead, the loads make the compiler wait for all of them (vmcnt(0))
-// before every later ds_read_b64_tr_b16 of the wave, whatever LDS it reads:
-// in a double-buffered tile loop that is a wait for the next tile's prefetch
-// in the middle of the current tile.  The compiler does not know what the
-// assembly writes, so every tile is read only after the wait_vmem() and the
-// workgroup barrier that follow its loads (as all callers do).  The assembly
-// also orders every other memory access of the kernel around it, which costs
-// registers in some kernels: each kernel takes the form measured faster.
+// Direct global->LDS loads through inline assembly (DmaPlan modes kDmaAsm
+// and kDmaAsmCast, dma_row_f32).  Lane i's SIZE bytes from `g` land at LDS
+// byte address m0 + i * SIZE, with m0 the wave-uniform `lds_base`.  Issued
+// through the builtin instead, the loads make the compiler wait for all of
+// them (vmcnt(0)) before every later ds_read_b64_tr_b16 of the wave, whatever
+// LDS it reads: in a double-buffered tile loop that is a wait for the next
+// tile's prefetch in the middle of the current tile.  The compiler does not
+// know what the assembly writes, so every tile is read only after the
+// wait_vmem() and the workgroup barrier that follow its loads (as all callers
+// do).  Register allocation differs between the forms, so each kernel takes
+// the one measured faster.
+enum DmaMode {
+    kDmaBuiltin = 0,  // __builtin_amdgcn_global_load_lds
+    kDmaAsm = 1,      // assembly; the wave's LDS slots from scalar arithmetic
+    kDmaAsmCast = 2,  // assembly; each slot's LDS address through an address-space cast
+};
+
+// LDS byte address of a generic pointer into LDS, wave-uniform: the low 32
+// bits of a flat LDS address are its LDS address (the shared aperture is
+// 4 GiB aligned), so no null check of an address-space cast is needed.
 __device__ __forceinline__ uint32_t lds_base_sgpr(const void *p)
 {
-    const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(to_lds(p)));
-    return __builtin_amdgcn_readfirstlane(a);
+    return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p)));
+}
+
+// The same through an address-space cast (generic null maps to -1).
+__device__ __forceinline__ uint32_t lds_base_cast(const void *p)
+{
+    return __builtin_amdgcn_readfirstlane(
+        static_cast<uint32_t>(reinterpret_cast<uintptr_t>(to_lds(p))));
 }
 
 __device__ __forceinline__ void dma_b128(const void *g, uint32_t lds_base)
@@ -94,7 +109,7 @@ __device__ __forceinline__ void dma_b32(const void *g, uint32_t lds_base)
 // that runs past row L-1 takes a slow path that clamps rows to L-1 (their
 // values are finite and the mask removes them).  Completion is tracked by
 // vmcnt.
-template <int D, int ROWS, int NW, bool ASM = false>
+template <int D, int ROWS, int NW, int MODE = kDmaBuiltin>
 struct DmaPlan {
     static constexpr int CPR = D / 8;               // chunks per row
     static constexpr int INSTRS = ROWS * CPR / 64;  // wave instructions per tile
@@ -115,12 +130,21 @@ struct DmaPlan {
     __device__ __forceinline__ void issue(uint16_t *lds_tile, const uint16_t *__restrict__ g,
                                           long long rs, int row0, int L, int wave, int lane) const
     {
+        // kDmaAsm: the wave's first 1 KiB slot of the tile, in SGPRs.
+        const uint32_t lslot =
+            MODE == kDmaAsm ? lds_base_sgpr(lds_tile) +
+                                  1024u * static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave))
+                            : 0u;
+        auto slot = [&](int k) __attribute__((always_inline)) -> uint32_t {
+            return MODE == kDmaAsm ? lslot + 1024u * NW * k
+                                   : lds_base_cast(lds_tile + (wave + NW * k) * 512);
+        };
         if (row0 + ROWS <= L) {
             const char *gb = reinterpret_cast<const char *>(g + row0 * rs);
 #pragma unroll
             for (int k = 0; k < PER; ++k) {
-                if constexpr (ASM)
-                    dma_b128_off(gb, off[k], lds_base_sgpr(lds_tile + (wave + NW * k) * 512));
+                if constexpr (MODE != kDmaBuiltin)
+                    dma_b128_off(gb, off[k], slot(k));
                 else
                     __builtin_amdgcn_global_load_lds(gb + off[k],
                                                      to_lds(lds_tile + (wave + NW * k) * 512), 16,
@@ -132,8 +156,8 @@ struct DmaPlan {
                 const int q = (wave + NW * k) * 64 + lane;
                 const int r = q / CPR, x = (q % CPR) ^ swz<D>(r);
                 const int row = min(row0 + r, L - 1);
-                if constexpr (ASM)
-                    dma_b128(g + row * rs + x * 8, lds_base_sgpr(lds_tile + (wave + NW * k) * 512));
+                if constexpr (MODE != kDmaBuiltin)
+                    dma_b128(g + row * rs + x * 8, slot(k));
                 else
                     __builtin_amdgcn_global_load_lds(g + row * rs + x * 8,
                                                      to_lds(lds_tile + (wave + NW * k) * 512), 16,
@@ -145,13 +169,15 @@ struct DmaPlan {
 
 // Direct-to-LDS load of ROWS consecutive fp32 values (ROWS == 64: one wave
 // instruction of 4-byte slots), rows clamped to L-1.
-template <bool ASM>
+template <int MODE>
 __device__ __forceinline__ void dma_row_f32(float *lds, const float *__restrict__ g, int row0,
                                             int L, int lane)
 {
     const int row = min(row0 + lane, L - 1);
-    if constexpr (ASM)
+    if constexpr (MODE == kDmaAsm)
         dma_b32(g + row, lds_base_sgpr(lds));
+    else if constexpr (MODE == kDmaAsmCast)
+        dma_b32(g + row, lds_base_cast(lds));
     else
         __builtin_amdgcn_global_load_lds(g + row, to_lds(lds), 4, 0, 0);
 }

@@ -1,9 +1,10 @@
 """Code-generation checks of the attention kernels (CPU: hipcc cross-compiles
 for gfx950; nothing runs on a GPU).
 
-* The kernels whose tile loads go through inline assembly (the dK/dV kernels
-  and the one-block D = 64 forward) must not wait for outstanding vector
-  memory operations (`s_waitcnt vmcnt`) right before a transposed LDS read:
+* The kernels whose tile loads go through inline assembly (forward, dQ, the
+  D = 64 dK/dV kernel and the one-block D = 128 dK/dV kernel) must not wait
+  for outstanding vector memory operations (`s_waitcnt vmcnt`) right before a
+  transposed LDS read:
   that wait is the one the builtin load made the compiler insert, for the
   next tile's prefetch in the middle of the current tile.
 * Register budgets the launch shapes rely on: no spills in any attention
@@ -69,8 +70,14 @@ def waits_before_transposed_reads(lines):
 @pytest.mark.parametrize("src, prefix", [
     ("dd_bwd.hip", "_ZN2dd12dkdv1_kernelILi64ELb0E"),
     ("dd_bwd.hip", "_ZN2dd12dkdv1_kernelILi64ELb1E"),
+    ("dd_bwd.hip", "_ZN2dd9dq_kernelILi64ELb0E"),
+    ("dd_bwd.hip", "_ZN2dd9dq_kernelILi64ELb1E"),
+    ("dd_bwd.hip", "_ZN2dd9dq_kernelILi128ELb0E"),
     ("dd_dkdv.hip", "_ZN2dd11dkdv_kernelILi128ELb0E"),
     ("dd_fwd.hip", "_ZN2dd10fwd_kernelILi64ELb0ELb0E"),
+    ("dd_fwd.hip", "_ZN2dd10fwd_kernelILi64ELb1ELb0E"),
+    ("dd_fwd.hip", "_ZN2dd10fwd_kernelILi128ELb0ELb0E"),
+    ("dd_fwd.hip", "_ZN2dd10fwd_kernelILi128ELb1ELb0E"),
 ])
 def test_no_dma_wait_before_transposed_reads(src, prefix, tmp_path):
     asm = device_asm(src, tmp_path)
