@@ -201,20 +201,22 @@ __device__ __forceinline__ void store_block_bf16(uint16_t *dst, const f32x16 &ac
     }
 }
 
-// Wave-wide min / max of an int.
+// Wave-wide min / max of an int.  Every lane ends with the same value; the
+// result is taken from lane 0 so that the compiler keeps it in a scalar
+// register.
 __device__ __forceinline__ int wave_min(int v)
 {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1)
         v = min(v, __shfl_xor(v, o));
-    return v;
+    return __builtin_amdgcn_readfirstlane(v);
 }
 __device__ __forceinline__ int wave_max(int v)
 {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1)
         v = max(v, __shfl_xor(v, o));
-    return v;
+    return __builtin_amdgcn_readfirstlane(v);
 }
 
 // A compile-time int as a type, to select a branch of a generic lambda.

@@ -87,8 +87,11 @@ __device__ __forceinline__ FwdItem fwd_item(int bid, int nqb, int B, int L, int 
 // fragments right after loading them (positions and frequencies as
 // dd_rope, so the result is bit-identical to a dd_rope pass) and, when
 // Qrot is not null, writes the rotated rows there for the backward.
+// Waves per SIMD: four in the one-block D = 64 form (at most 128 VGPRs),
+// three in the persistent one (its LDS holds three workgroups per CU), two
+// at D = 128.
 template <int D, bool PERSIST, bool ROPE>
-__global__ void __launch_bounds__(256, D == 64 ? 3 : 2)
+__global__ void __launch_bounds__(256, D == 64 ? (PERSIST ? 3 : 4) : 2)
 fwd_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
            const uint16_t *__restrict__ V, uint16_t *__restrict__ O, float *__restrict__ LSE,
            int B, int L, int H, int causal_i, const int32_t *__restrict__ cu, int n_docs,

@@ -8,7 +8,7 @@ for gfx950; nothing runs on a GPU).
   that wait is the one the builtin load made the compiler insert, for the
   next tile's prefetch in the middle of the current tile.
 * Register budgets the launch shapes rely on: no spills in any attention
-  kernel, and the one-block D = 64 forward within 168 VGPRs (three waves per
+  kernel, and the one-block D = 64 forward within 128 VGPRs (four waves per
   SIMD).
 """
 import os
@@ -94,4 +94,4 @@ def test_attention_kernels_do_not_spill(src, tmp_path):
     assert not spills, spills
     if src == "dd_fwd.hip":
         sym = next(k for k in res if k.startswith("_ZN2dd10fwd_kernelILi64ELb0ELb0E"))
-        assert res[sym][0] <= 168, res[sym]
+        assert res[sym][0] <= 128, res[sym]
