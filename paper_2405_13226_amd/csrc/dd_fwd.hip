@@ -43,10 +43,13 @@ struct FwdTile {
 // unchanged.
 constexpr float kRescaleSlack = 8.0f;
 
-// Row lengths (tokens) up to which the forward runs persistently.  The test
-// ignores document masking: documents make the work per query block uneven,
-// which hardware dispatch balances and a fixed walk order does not.
-constexpr long long kFwdPersistMaxSpan = 2048;
+// Row lengths (tokens) up to which the forward runs persistently: 1024 at
+// D = 64 (the one-block form, four waves per SIMD, is faster from 2048 on),
+// 2048 at D = 128.  The test ignores document masking: documents make the
+// work per query block uneven, which hardware dispatch balances and a fixed
+// walk order does not.
+template <int D>
+constexpr long long kFwdPersistMaxSpan = D == 64 ? 1024 : 2048;
 
 // A query-block work item of the forward: one block of FwdTile::BM queries of
 // one (b, h) slice and the key tiles those queries see.
@@ -443,7 +446,7 @@ static int launch_fwd_d(const FwdArgs &a)
     const RopeEpi rt = ROPE ? rope_epi(a.rope_base, D) : RopeEpi{};
     // Persistent for short rows: as many workgroups as are resident at once.
     const long long pgrid =
-        a.L <= kFwdPersistMaxSpan ? persistent_grid<fwd_kernel<D, true, ROPE>>(256) : 0;
+        a.L <= kFwdPersistMaxSpan<D> ? persistent_grid<fwd_kernel<D, true, ROPE>>(256) : 0;
     const bool persist = pgrid > 0 && pgrid < all;
     ProfScope prof(K_FWD, static_cast<hipStream_t>(a.stream));
     const hipError_t e = launch_kernel(
