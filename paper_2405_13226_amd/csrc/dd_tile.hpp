@@ -85,7 +85,8 @@ __device__ __forceinline__ void dma_b128(const void *g, uint32_t lds_base)
 }
 
 // The same with a wave-uniform base address and a 32-bit per-lane byte
-// offset (no 64-bit address arithmetic per load).
+// offset (no 64-bit address arithmetic per load).  The offsets of a tile
+// fit: at most 256 rows of H * D < 2^23 elements of 2 bytes.
 __device__ __forceinline__ void dma_b128_off(const void *base, uint32_t off, uint32_t lds_base)
 {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
