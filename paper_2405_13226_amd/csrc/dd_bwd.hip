@@ -341,8 +341,10 @@ __device__ __forceinline__ QItem q_item(int bid, int nqb, int B, int L, int H, b
 // it DMAs the next block's first K/V tile into the free stage and the next
 // block's Q and dO rows into LDS areas of their own (read into registers
 // after that tile), and loads its O rows and LSE into registers.
+// Waves per SIMD: four in the one-block D = 64 form (at most 128 VGPRs),
+// two otherwise (the persistent form's item loop and D = 128 need more).
 template <int D, bool PERSIST>
-__global__ void __launch_bounds__(256, 2)
+__global__ void __launch_bounds__(256, (D == 64 && !PERSIST) ? 4 : 2)
 dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
           const uint16_t *__restrict__ V, const uint16_t *__restrict__ O,
           const uint16_t *__restrict__ dO, const float *__restrict__ LSE,
@@ -540,10 +542,10 @@ dq_kernel(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
             if (MASKED && (j0 + 32 * kb > hi_w || j0 + 32 * kb + 31 < lo_w))
                 continue;
             // The A fragments are read in batches of KB_STEP k-steps before
-            // their products, so several LDS reads are in flight at once
-            // (two at D = 64, which keeps the kernel at 163 VGPRs, three
-            // waves per SIMD).
-            constexpr int KB_STEP = KK >= 8 ? 4 : 2;
+            // their products, so several LDS reads are in flight at once; in
+            // the one-block D = 64 form one k-step at a time keeps the kernel
+            // within 128 VGPRs, four waves per SIMD.
+            constexpr int KB_STEP = KK >= 8 ? 4 : (PERSIST ? 2 : 1);
             // dP^T accumulates onto -delta (this lane's query), so the
             // products give dP - delta, and the fill runs beside the S
             // products instead of a subtraction after them.  The opaque copy

@@ -152,12 +152,18 @@ struct DmaPlan {
                                                      0, 0);
             }
         } else {
+            // kDmaAsm: offsets from row min(row0, L-1), never negative and
+            // below ROWS rows (a 64-bit address per lane would hold VGPRs).
+            const int rb = min(row0, L - 1);
+            const char *gr = reinterpret_cast<const char *>(g + rb * rs);
 #pragma unroll
             for (int k = 0; k < PER; ++k) {
                 const int q = (wave + NW * k) * 64 + lane;
                 const int r = q / CPR, x = (q % CPR) ^ swz<D>(r);
                 const int row = min(row0 + r, L - 1);
-                if constexpr (MODE != kDmaBuiltin)
+                if constexpr (MODE == kDmaAsm)
+                    dma_b128_off(gr, static_cast<uint32_t>(((row - rb) * rs + x * 8) * 2), slot(k));
+                else if constexpr (MODE == kDmaAsmCast)
                     dma_b128(g + row * rs + x * 8, slot(k));
                 else
                     __builtin_amdgcn_global_load_lds(g + row * rs + x * 8,

@@ -8,8 +8,8 @@ for gfx950; nothing runs on a GPU).
   that wait is the one the builtin load made the compiler insert, for the
   next tile's prefetch in the middle of the current tile.
 * Register budgets the launch shapes rely on: no spills in any attention
-  kernel, and the one-block D = 64 forward within 128 VGPRs (four waves per
-  SIMD).
+  kernel, and the one-block D = 64 forward and dQ kernels within 128 VGPRs
+  (four waves per SIMD).
 """
 import os
 import re
@@ -92,6 +92,8 @@ def test_attention_kernels_do_not_spill(src, tmp_path):
     assert res, src
     spills = {k: v for k, v in res.items() if v[1] != 0}
     assert not spills, spills
-    if src == "dd_fwd.hip":
-        sym = next(k for k in res if k.startswith("_ZN2dd10fwd_kernelILi64ELb0ELb0E"))
+    four_waves = {"dd_fwd.hip": "_ZN2dd10fwd_kernelILi64ELb0ELb0E",
+                  "dd_bwd.hip": "_ZN2dd9dq_kernelILi64ELb0E"}
+    if src in four_waves:
+        sym = next(k for k in res if k.startswith(four_waves[src]))
         assert res[sym][0] <= 128, res[sym]
